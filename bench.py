@@ -1,0 +1,230 @@
+"""Throughput of the PAM matrix-product hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload w5]
+
+One step runs every product of the workload once (for the default large
+linear layer: forward Y = X .^ W^T, dX = dY .^ W and dW = dY^T .^ X) on
+seeded synthetic inputs already resident in HBM.  K steps are timed between
+device synchronisations; the printed JSON line reports whole-job PAM-MAC/s
+(one PAM-MAC = one piecewise affine product + one float32 accumulate), the
+vector-ALU roofline of the dominant kernel measured with HIP events on the
+launch stream, and the CPU oracle timed on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# Minimum vector-ALU lane operations per PAM-MAC on gfx950: one int32 add of
+# the two encodings (one operand pre-biased once per LDS chunk) and one
+# float32 add.
+ALGO_LANE_OPS_PER_MAC = 2
+# MI355X nominal: 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz.
+NOMINAL_VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2305_17190_amd", "csrc", "pam_kernels.hip")
+
+
+def log(msg: str) -> None:
+    sys.stderr.write(msg + "\n")
+    sys.stderr.flush()
+
+
+def kernel_source_digest() -> str:
+    with open(KERNEL_SOURCE, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def committed_traffic(workload: str, form: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary.
+
+    Returns None when there is no summary for this kernel or the kernel
+    source changed since the counters were taken.
+    """
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}_{form}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    sha = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not val or sha.group(1) != kernel_source_digest():
+        return None
+    return float(val.group(1))
+
+
+def cpu_baseline(workload_id: int, host, forms, target_s: float) -> dict:
+    """Time the C oracle on a bounded slice of every product of the workload."""
+    import numpy as np
+    from oracle import pam_c
+
+    pam_c.load()
+    threads = pam_c.num_threads()
+
+    def run(form, count):
+        a, b = host[form.a], host[form.b]
+        if form.batch > 1:
+            bats = list(range(count))
+            t0 = time.perf_counter()
+            pam_c.pam_gemm(a, b, form.trans_a, form.trans_b, form.m, form.n, form.k, form.lda, form.ldb,
+                           form.stride_a, form.stride_b, batches=bats)
+            return time.perf_counter() - t0, count * form.m * form.n * form.k
+        rows = list(range(count))
+        t0 = time.perf_counter()
+        pam_c.pam_gemm(a, b, form.trans_a, form.trans_b, form.m, form.n, form.k, form.lda, form.ldb, rows=rows)
+        return time.perf_counter() - t0, count * form.n * form.k
+
+    # Probe with a small slice per product, then scale the slice to the target time.
+    per_form = target_s / len(forms)
+    total_t, total_macs, parts = 0.0, 0, []
+    for form in forms:
+        limit = form.batch if form.batch > 1 else form.m
+        count = min(limit, max(1, threads))
+        t, macs = run(form, count)
+        if t < per_form / 4:
+            count = min(limit, max(count, int(count * per_form / max(t, 1e-3))))
+            t, macs = run(form, count)
+        total_t += t
+        total_macs += macs
+        parts.append(f"{form.name}: {count} {'batch entries' if form.batch > 1 else 'rows'}")
+    return {
+        "value": total_macs / total_t / 1e9,
+        "unit": "GPAM-MAC/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"workload {workload_id} ({'; '.join(parts)}), C oracle, float64 accumulate, "
+                  f"{total_macs:.3e} PAM-MACs in {total_t:.1f} s",
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="w5", choices=["w1", "w2", "w3", "w4", "w5"])
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the PAM matrix product is "
+              "built and measured on a single MI355X.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import pam_workloads as wl
+    import paper_2305_17190_amd as pam
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        return 1
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    pam.load()
+
+    wid = int(args.workload[1:])
+    spec = wl.WORKLOADS[wid]
+    forms = spec["forms"]
+    log(f"generating workload {wid} ({spec['desc']})")
+    host = wl.workload_inputs(wid)
+    dt = {k: torch.from_numpy(v).to(dev) for k, v in host.items()}
+    outs = {}
+    for f in forms:
+        shape = (f.batch, f.m, f.n) if f.batch > 1 else (f.m, f.n)
+        outs[f.name] = torch.empty(shape, dtype=torch.float32, device=dev)
+
+    def launch(f):
+        if f.batch > 1:
+            pam.bmm(dt[f.a], dt[f.b], trans_a=f.trans_a, trans_b=f.trans_b, out=outs[f.name])
+        else:
+            pam.gemm(dt[f.a], dt[f.b], trans_a=f.trans_a, trans_b=f.trans_b, out=outs[f.name])
+
+    macs_per_step = sum(f.macs for f in forms)
+    for _ in range(args.warmup):
+        for f in forms:
+            launch(f)
+    torch.cuda.synchronize()
+
+    events = {f.name: [] for f in forms}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        for f in forms:
+            s = torch.cuda.Event(enable_timing=True)
+            e = torch.cuda.Event(enable_timing=True)
+            s.record()
+            launch(f)
+            e.record()
+            events[f.name].append((s, e))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    per_form = {}
+    for f in forms:
+        ms = [s.elapsed_time(e) for s, e in events[f.name]]
+        per_form[f.name] = sum(ms) / len(ms)
+        log(f"  {f.name:6s} m={f.m} n={f.n} k={f.k} batch={f.batch} plan={pam.plan(f.m, f.n, f.k, f.batch)} "
+            f"avg {per_form[f.name]:.3f} ms  {f.macs / per_form[f.name] / 1e9:.1f} GPAM-MAC/s")
+
+    info = pam.device_info(0)
+    peak = NOMINAL_VALU_LANE_OPS
+    dom = max(forms, key=lambda f: per_form[f.name] * 1.0)
+    dom_s = per_form[dom.name] / 1e3
+    achieved = ALGO_LANE_OPS_PER_MAC * dom.macs / dom_s
+    value = macs_per_step * args.steps / elapsed / 1e9
+    log(f"device: {info}")
+    log(f"step {elapsed / args.steps * 1e3:.3f} ms, {value:.1f} GPAM-MAC/s; dominant {dom.name}: "
+        f"{achieved / 1e12:.2f} of {peak / 1e12:.2f} Tlane-op/s (device-read peak "
+        f"{info['valu_lane_ops_per_s'] / 1e12:.2f})")
+
+    result = {
+        "metric": "PAM-GEMM G PAM-MAC/s on one MI355X; % of VALU op-rate peak",
+        "value": round(value, 3),
+        "unit": "GPAM-MAC/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": spec["name"],
+            "products": [f"{f.name} ({'T' if f.trans_a else 'N'}{'T' if f.trans_b else 'N'}) "
+                         f"{f.batch}x{f.m}x{f.n}x{f.k}" for f in forms],
+            "pam_macs_per_step": macs_per_step,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "alu",
+            "kernel": f"pam_gemm_kernel {dom.name} ({'T' if dom.trans_a else 'N'}{'T' if dom.trans_b else 'N'})",
+            "achieved": round(achieved / 1e12, 3),
+            "peak": round(peak / 1e12, 3),
+            "unit": "Tlane-op/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": committed_traffic(spec["name"], dom.name),
+            "lane_ops_per_mac": ALGO_LANE_OPS_PER_MAC,
+            "avg_launch_ms": round(per_form[dom.name], 4),
+            "device_peak": round(info["valu_lane_ops_per_s"] / 1e12, 3),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(wid, host, forms, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,157 @@
+/*
+ * pam.h -- C ABI of the piecewise affine multiplication (PAM) library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: Kosson & Jaggi, "Multiplication-Free Transformer Training via
+ * Piecewise Affine Operations" (NeurIPS 2023).
+ *
+ * PAM (Sec. 2.2) replaces the product of two float32 numbers
+ *   A = (-1)^S_A 2^E_A (1 + M_A),  B = (-1)^S_B 2^E_B (1 + M_B)
+ * by (-1)^(S_A+S_B) 2^(E_A+E_B+c) (1 + M_A + M_B - c), c = 1{M_A + M_B >= 1},
+ * which is the int32 sum of the two encodings minus one exponent bias
+ * (127 << 23).  The same passage asks for clamped exponent under/overflow,
+ * flushed denormals and explicit NaN/inf handling; this library fixes those
+ * cases as follows (identical in every entry point):
+ *   - sign of the result = exclusive or of the operand signs, also for zeros;
+ *   - a zero or denormal operand gives a signed zero;
+ *   - a result whose exponent field would be <= 0 is a signed zero;
+ *   - a result whose exponent field would be >= 255 is +-FLT_MAX;
+ *   - a NaN operand, or inf times a zero/denormal, gives 0x7FC00000;
+ *     inf times any other value gives a signed inf.
+ *
+ * PAM matrix products (Sec. 3.2, Table 1 approximate derivative) replace
+ * every scalar product of a matrix multiply by PAM and keep ordinary float32
+ * addition for the accumulation (App. "Hardware Cost", App. "PAM with
+ * Narrower Mantissas").  The summation order is not part of the contract:
+ * results agree with an exact-order sum to within float32 rounding, and
+ * denormal partial sums may be flushed to zero.
+ *
+ * Conventions for every call:
+ *   - All matrix/array pointers are DEVICE pointers (memory of the current
+ *     HIP device); the caller owns every buffer.
+ *   - Every call is asynchronous on `stream` (NULL = the null stream) and
+ *     never synchronises.  Execution errors surface at the caller's next
+ *     synchronisation.
+ *   - Matrices are row-major with leading dimensions in elements.  For a
+ *     matrix product, op(A) is m x k and op(B) is k x n:
+ *       op(A)(i, p) = A[i*lda + p]  if transA == PAM_OP_N,  A[p*lda + i]  if PAM_OP_T
+ *       op(B)(p, j) = B[p*ldb + j]  if transB == PAM_OP_N,  B[j*ldb + p]  if PAM_OP_T
+ *     and C(i, j) = C[i*ldc + j] is overwritten (there is no alpha/beta:
+ *     scaling would be a multiplication).
+ *   - Arguments are validated before anything is launched; on failure the
+ *     call returns PAM_ERROR_INVALID_VALUE and pam_last_error() says why.
+ *   - Output regions overlapping an input are undefined (not checked), except
+ *     that pam_mul may run in place (out == a or out == b).
+ *   - Split-K plans take a temporary partial-sum buffer from the
+ *     stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`);
+ *     nothing stays allocated when the call returns.
+ */
+#ifndef PAM_H_
+#define PAM_H_
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PAM_SUCCESS = 0,
+    PAM_ERROR_INVALID_VALUE = 1, /* bad size, leading dimension, pointer or option */
+    PAM_ERROR_LAUNCH = 2,        /* a HIP launch or query failed */
+    PAM_ERROR_NOT_SUPPORTED = 3, /* device is not gfx950 */
+    PAM_ERROR_ALLOC = 4          /* stream-ordered workspace allocation failed */
+} pam_status_t;
+
+typedef enum { PAM_OP_N = 0, PAM_OP_T = 1 } pam_op_t;
+
+/*
+ * Elementwise PAM (Sec. 2.2): out[i] = a[i] .^ b[i] for 0 <= i < n.
+ * a, b, out: device arrays of n float32.  n >= 0 (n == 0 launches nothing).
+ * Bit-exact: every one of the 2^64 operand pairs has exactly one result.
+ */
+pam_status_t pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
+
+/*
+ * PAM matrix product (Sec. 3.2): C(i, j) = sum_p op(A)(i, p) .^ op(B)(p, j)
+ * for 0 <= i < m, 0 <= j < n, float32 accumulation.
+ * The forward pass of a linear layer Y = X W^T is (N, T); its approximate
+ * backward products (Table 1) are dX = dY W (N, N) and dW = dY^T X (T, N).
+ * Requirements: m, n, k >= 0; lda >= max(1, transA == N ? k : m);
+ * ldb >= max(1, transB == N ? n : k); ldc >= max(1, n); A, B non-NULL when
+ * m*k resp. k*n > 0; C non-NULL when m*n > 0.  m == 0 or n == 0 launches
+ * nothing; k == 0 writes +0.0f to C.
+ */
+pam_status_t pam_gemm(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                      const float *A, int64_t lda, const float *B, int64_t ldb,
+                      float *C, int64_t ldc, hipStream_t stream);
+
+/*
+ * `batch` independent PAM matrix products, as in the attention products of
+ * Sec. 3.2 (Q K^T, P V and their backward products).  Product z reads
+ * A + z*strideA and B + z*strideB and writes C + z*strideC, each with the
+ * layout of pam_gemm.  Strides are in elements, >= 0 (a zero A or B stride
+ * broadcasts that operand); batch >= 0.  Same requirements as pam_gemm.
+ */
+pam_status_t pam_gemm_batched(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                              const float *A, int64_t lda, int64_t strideA,
+                              const float *B, int64_t ldb, int64_t strideB,
+                              float *C, int64_t ldc, int64_t strideC,
+                              int64_t batch, hipStream_t stream);
+
+/*
+ * How a product is tiled: output tile tile_m x tile_n per workgroup, and the
+ * number of K slices whose partial sums are added afterwards (1 = none).
+ */
+typedef struct {
+    int32_t tile_m;
+    int32_t tile_n;
+    int32_t splits;
+} pam_plan_t;
+
+/* The plan pam_gemm / pam_gemm_batched would use for these sizes. */
+pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_plan_t *plan);
+
+/*
+ * pam_gemm_batched with an explicit plan (for tests and tuning).
+ * tile_m, tile_n in {64, 128}; splits >= 1.  The result is the same
+ * product as with the automatic plan, up to float32 summation order.
+ */
+pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB,
+                                        int64_t m, int64_t n, int64_t k,
+                                        const float *A, int64_t lda, int64_t strideA,
+                                        const float *B, int64_t ldb, int64_t strideB,
+                                        float *C, int64_t ldc, int64_t strideC,
+                                        int64_t batch, const pam_plan_t *plan,
+                                        hipStream_t stream);
+
+/*
+ * Figures of `device` that set the vector-ALU roofline: compute units,
+ * SIMDs per compute unit, lanes each SIMD retires per clock, peak engine
+ * clock (kHz) and wavefront size, read from the HIP runtime and HSA.
+ * valu_lane_ops_per_s = cus * simds_per_cu * lanes_per_simd * clock.
+ */
+typedef struct {
+    int32_t compute_units;
+    int32_t simds_per_cu;
+    int32_t lanes_per_simd;
+    int32_t clock_khz;
+    int32_t wavefront_size;
+    double valu_lane_ops_per_s;
+    char arch[64];
+} pam_device_info_t;
+
+pam_status_t pam_device_info(int device, pam_device_info_t *info);
+
+/* Static text for a status code. */
+const char *pam_status_string(pam_status_t status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char *pam_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAM_H_ */

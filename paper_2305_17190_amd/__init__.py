@@ -1,0 +1,207 @@
+"""Piecewise affine multiplication (PAM) on AMD Instinct MI355X (gfx950).
+
+Thin Python binding over the C ABI in ``include/pam.h`` (libpam.so, built
+from ``csrc/``).  The binding only marshals arguments: every step of the
+computation runs in the library's HIP kernels, on the caller's current HIP
+stream.  There is no CPU fallback; without the built library or a gfx950
+device every call raises.
+
+    mul(a, b, out=None)                        elementwise a .^ b
+    gemm(A, B, trans_a, trans_b, out=None)     C = op(A) .^ op(B)
+    bmm(A, B, trans_a, trans_b, out=None)      batched over the leading axis
+
+Matrix arguments are float32 HIP tensors whose last dimension is contiguous
+(row stride = leading dimension).  op(X) = X^T when trans_x is True.  The
+linear layer Y = X W^T is ``gemm(X, W, trans_b=True)``; its backward
+products (approximate derivative, Table 1 of the paper) are
+``gemm(dY, W)`` and ``gemm(dY, X, trans_a=True)``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+__all__ = ["mul", "gemm", "bmm", "plan", "device_info", "library_path", "load", "PamError"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpam.so")
+
+PAM_OP_N, PAM_OP_T = 0, 1
+
+
+class PamError(RuntimeError):
+    pass
+
+
+class _Plan(ctypes.Structure):
+    _fields_ = [("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("splits", ctypes.c_int32)]
+
+
+class _DeviceInfo(ctypes.Structure):
+    _fields_ = [("compute_units", ctypes.c_int32), ("simds_per_cu", ctypes.c_int32),
+                ("lanes_per_simd", ctypes.c_int32), ("clock_khz", ctypes.c_int32),
+                ("wavefront_size", ctypes.c_int32), ("valu_lane_ops_per_s", ctypes.c_double),
+                ("arch", ctypes.c_char * 64)]
+
+
+_lib = None
+
+# Every symbol include/pam.h declares.
+EXPORTS = ("pam_mul", "pam_gemm", "pam_gemm_batched", "pam_gemm_plan", "pam_gemm_batched_with_plan",
+           "pam_device_info", "pam_status_string", "pam_last_error")
+
+
+def library_path() -> str:
+    return LIB_PATH
+
+
+def load() -> ctypes.CDLL:
+    """Load libpam.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise PamError(f"{LIB_PATH} is missing: build it with `python -m paper_2305_17190_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    lib.pam_mul.argtypes = [vp, vp, vp, i64, vp]
+    lib.pam_gemm.argtypes = [i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp]
+    lib.pam_gemm_batched.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, vp]
+    lib.pam_gemm_batched_with_plan.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64,
+                                               i64, ctypes.POINTER(_Plan), vp]
+    lib.pam_gemm_plan.argtypes = [i64, i64, i64, i64, ctypes.POINTER(_Plan)]
+    lib.pam_device_info.argtypes = [i32, ctypes.POINTER(_DeviceInfo)]
+    for name in ("pam_mul", "pam_gemm", "pam_gemm_batched", "pam_gemm_batched_with_plan", "pam_gemm_plan",
+                 "pam_device_info"):
+        getattr(lib, name).restype = i32
+    lib.pam_status_string.argtypes = [i32]
+    lib.pam_status_string.restype = ctypes.c_char_p
+    lib.pam_last_error.argtypes = []
+    lib.pam_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        lib = load()
+        raise PamError(f"{lib.pam_status_string(status).decode()}: {lib.pam_last_error().decode()}")
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(t) -> int:
+    torch = _torch()
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _require(t, name: str, ndim: int):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32, got {t.dtype}")
+    if not t.is_cuda:
+        raise PamError(f"{name} must be a HIP (cuda) tensor; the PAM library has no CPU path")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got {t.dim()}")
+    if t.numel() > 0 and t.stride(-1) != 1:
+        raise ValueError(f"{name} must have a contiguous last dimension")
+
+
+def mul(a, b, out=None):
+    """Elementwise PAM of two equally shaped contiguous float32 tensors."""
+    torch = _torch()
+    for name, t in (("a", a), ("b", b)):
+        _require(t, name, t.dim() if isinstance(t, torch.Tensor) else 1)
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if a.shape != b.shape:
+        raise ValueError(f"shape mismatch {tuple(a.shape)} vs {tuple(b.shape)}")
+    if out is None:
+        out = torch.empty_like(a)
+    elif out.shape != a.shape or not out.is_contiguous() or out.dtype != torch.float32:
+        raise ValueError("out must be a contiguous float32 tensor of the same shape")
+    _check(load().pam_mul(a.data_ptr(), b.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
+    return out
+
+
+def _dims(A, B, trans_a: bool, trans_b: bool):
+    m, k = (A.shape[-1], A.shape[-2]) if trans_a else (A.shape[-2], A.shape[-1])
+    kb, n = (B.shape[-1], B.shape[-2]) if trans_b else (B.shape[-2], B.shape[-1])
+    if k != kb:
+        raise ValueError(f"inner dimensions differ: op(A) is {m}x{k}, op(B) is {kb}x{n}")
+    return m, n, k
+
+
+def _ld(t) -> int:
+    return max(int(t.stride(-2)), 1) if t.numel() > 0 else max(int(t.shape[-1]), 1)
+
+
+def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None):
+    """C = op(A) .^ op(B) with float32 accumulation; returns C (m x n)."""
+    torch = _torch()
+    _require(A, "A", 2)
+    _require(B, "B", 2)
+    m, n, k = _dims(A, B, trans_a, trans_b)
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    else:
+        _require(out, "out", 2)
+        if tuple(out.shape) != (m, n):
+            raise ValueError(f"out must be {m}x{n}")
+    _check(load().pam_gemm(PAM_OP_T if trans_a else PAM_OP_N, PAM_OP_T if trans_b else PAM_OP_N, m, n, k,
+                           A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
+                           _stream_handle(A)))
+    return out
+
+
+def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None):
+    """Batched C[z] = op(A[z]) .^ op(B[z]) over the leading axis.
+
+    ``plan`` = (tile_m, tile_n, splits) forces a tiling (tests and tuning).
+    """
+    torch = _torch()
+    _require(A, "A", 3)
+    _require(B, "B", 3)
+    if A.shape[0] != B.shape[0]:
+        raise ValueError("batch sizes differ")
+    batch = A.shape[0]
+    m, n, k = _dims(A, B, trans_a, trans_b)
+    if out is None:
+        out = torch.empty((batch, m, n), dtype=torch.float32, device=A.device)
+    else:
+        _require(out, "out", 3)
+        if tuple(out.shape) != (batch, m, n):
+            raise ValueError(f"out must be {batch}x{m}x{n}")
+    ta = PAM_OP_T if trans_a else PAM_OP_N
+    tb = PAM_OP_T if trans_b else PAM_OP_N
+    args = (ta, tb, m, n, k, A.data_ptr(), _ld(A), A.stride(0), B.data_ptr(), _ld(B), B.stride(0),
+            out.data_ptr(), _ld(out), out.stride(0), batch)
+    lib = load()
+    if plan is None:
+        _check(lib.pam_gemm_batched(*args, _stream_handle(A)))
+    else:
+        p = _Plan(*plan)
+        _check(lib.pam_gemm_batched_with_plan(*args, ctypes.byref(p), _stream_handle(A)))
+    return out
+
+
+def plan(m: int, n: int, k: int, batch: int = 1):
+    """(tile_m, tile_n, splits) the library picks for these sizes."""
+    p = _Plan()
+    _check(load().pam_gemm_plan(m, n, k, batch, ctypes.byref(p)))
+    return (p.tile_m, p.tile_n, p.splits)
+
+
+def device_info(device: int = 0) -> dict:
+    info = _DeviceInfo()
+    _check(load().pam_device_info(device, ctypes.byref(info)))
+    return {"compute_units": info.compute_units, "simds_per_cu": info.simds_per_cu,
+            "lanes_per_simd": info.lanes_per_simd, "clock_khz": info.clock_khz,
+            "wavefront_size": info.wavefront_size, "valu_lane_ops_per_s": info.valu_lane_ops_per_s,
+            "arch": info.arch.decode()}

@@ -1,0 +1,357 @@
+// C ABI of the PAM library: argument validation, plan selection, workspace
+// handling and launches.  The arithmetic lives in pam_kernels.hip.
+
+#include <hip/hip_runtime.h>
+#include <hsa/hsa.h>
+#include <hsa/hsa_ext_amd.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "pam.h"
+#include "pam_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+pam_status_t fail(pam_status_t s, const std::string &msg) {
+    g_last_error = msg;
+    return s;
+}
+
+pam_status_t fail_hip(hipError_t e, const char *what) {
+    g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+    return PAM_ERROR_LAUNCH;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int64_t kMaxDim = 0x7FFFFFFF;
+constexpr int64_t kMaxGridZ = 65535;
+constexpr int64_t kMaxSplits = 64;
+// Enough waves for about two per SIMD on a 256-CU device.
+constexpr int64_t kTargetWaves = 2048;
+
+struct Plan {
+    int tile_m, tile_n, splits;
+    int64_t k_per_split;
+};
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Largest tile whose padding waste is small, then split K until the launch
+// has enough waves (each split keeps at least four LDS chunks).
+Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch) {
+    static const int cand[3][2] = {{128, 128}, {128, 64}, {64, 64}};
+    int bm = 64, bn = 64;
+    for (const auto &c : cand) {
+        const double waste = double(ceil_div(m, c[0]) * c[0]) * double(ceil_div(n, c[1]) * c[1]) / double(m * n);
+        if (waste <= 1.15) {
+            bm = c[0];
+            bn = c[1];
+            break;
+        }
+    }
+    const int64_t waves = ceil_div(m, bm) * ceil_div(n, bn) * batch * (bm * bn / 4096);
+    int64_t splits = 1;
+    if (waves > 0 && waves < kTargetWaves) {
+        const int64_t want = ceil_div(2 * kTargetWaves, waves);
+        const int64_t most = std::max<int64_t>(1, k / (4 * pamk::kChunkK));
+        splits = std::min(std::min(want, most), kMaxSplits);
+    }
+    Plan p{bm, bn, 1, k};
+    if (splits > 1) {
+        const int64_t per = ceil_div(ceil_div(k, splits), pamk::kChunkK) * pamk::kChunkK;
+        p.k_per_split = per;
+        p.splits = (int)ceil_div(k, per);
+    }
+    return p;
+}
+
+pam_status_t validate(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                      int64_t sa, const float *B, int64_t ldb, int64_t sb, const float *C, int64_t ldc, int64_t sc,
+                      int64_t batch) {
+    char buf[256];
+    if ((ta != PAM_OP_N && ta != PAM_OP_T) || (tb != PAM_OP_N && tb != PAM_OP_T))
+        return fail(PAM_ERROR_INVALID_VALUE, "transA/transB must be PAM_OP_N or PAM_OP_T");
+    if (m < 0 || n < 0 || k < 0 || batch < 0) {
+        snprintf(buf, sizeof buf, "negative size (m=%lld n=%lld k=%lld batch=%lld)", (long long)m, (long long)n,
+                 (long long)k, (long long)batch);
+        return fail(PAM_ERROR_INVALID_VALUE, buf);
+    }
+    if (m > kMaxDim || n > kMaxDim || k > kMaxDim)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
+    if (sa < 0 || sb < 0 || sc < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "batch strides must be >= 0");
+    const int64_t min_lda = std::max<int64_t>(1, ta == PAM_OP_N ? k : m);
+    const int64_t min_ldb = std::max<int64_t>(1, tb == PAM_OP_N ? n : k);
+    const int64_t min_ldc = std::max<int64_t>(1, n);
+    if (lda < min_lda || ldb < min_ldb || ldc < min_ldc) {
+        snprintf(buf, sizeof buf, "leading dimension too small (lda=%lld>=%lld ldb=%lld>=%lld ldc=%lld>=%lld)",
+                 (long long)lda, (long long)min_lda, (long long)ldb, (long long)min_ldb, (long long)ldc,
+                 (long long)min_ldc);
+        return fail(PAM_ERROR_INVALID_VALUE, buf);
+    }
+    if (batch > 0) {
+        if (m * k > 0 && A == nullptr)
+            return fail(PAM_ERROR_INVALID_VALUE, "A is NULL");
+        if (k * n > 0 && B == nullptr)
+            return fail(PAM_ERROR_INVALID_VALUE, "B is NULL");
+        if (m * n > 0 && C == nullptr)
+            return fail(PAM_ERROR_INVALID_VALUE, "C is NULL");
+    }
+    return PAM_SUCCESS;
+}
+
+pam_status_t check_device() {
+    static thread_local int checked_device = -1;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return fail_hip(e, "hipGetDevice");
+    if (dev == checked_device)
+        return PAM_SUCCESS;
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess)
+        return fail_hip(e, "hipGetDeviceProperties");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(PAM_ERROR_NOT_SUPPORTED, std::string("device is ") + prop.gcnArchName + ", library built for gfx950");
+    // Keep freed split-K workspaces in the stream-ordered pool instead of
+    // returning them to the driver at every synchronisation.
+    hipMemPool_t pool = nullptr;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess && pool != nullptr) {
+        uint64_t threshold = UINT64_MAX;
+        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
+    }
+    checked_device = dev;
+    return PAM_SUCCESS;
+}
+
+pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                      int64_t sa, const float *B, int64_t ldb, int64_t sb, float *C, int64_t ldc, int64_t sc,
+                      int64_t batch, const Plan &plan, hipStream_t stream) {
+    if (m == 0 || n == 0 || batch == 0)
+        return PAM_SUCCESS;
+    pam_status_t st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    if (k == 0) {
+        for (int64_t b0 = 0; b0 < batch; b0 += kMaxGridZ) {
+            const int64_t nb = std::min(kMaxGridZ, batch - b0);
+            hipError_t e = pamk::launch_fill_zero(C + b0 * sc, (int32_t)m, (int32_t)n, ldc, sc, nb, stream);
+            if (e != hipSuccess)
+                return fail_hip(e, "fill kernel launch");
+        }
+        return PAM_SUCCESS;
+    }
+
+    pamk::GemmParams p{};
+    p.lda = lda;
+    p.ldb = ldb;
+    p.ldc = ldc;
+    p.strideA = sa;
+    p.strideB = sb;
+    p.strideC = sc;
+    p.m = (int32_t)m;
+    p.n = (int32_t)n;
+    p.k = (int32_t)k;
+    p.k_per_split = (int32_t)std::min<int64_t>(plan.k_per_split, kMaxDim);
+    p.splits = plan.splits;
+    p.tiles_n = (int32_t)ceil_div(n, plan.tile_n);
+    p.vec_a = aligned16(A) && lda % 4 == 0 && (batch == 1 || sa % 4 == 0);
+    p.vec_b = aligned16(B) && ldb % 4 == 0 && (batch == 1 || sb % 4 == 0);
+
+    const int64_t gz_max = kMaxGridZ;
+    float *ws = nullptr;
+    if (plan.splits > 1) {
+        const int64_t nb = std::min(batch, gz_max);
+        const size_t bytes = (size_t)nb * plan.splits * (size_t)m * (size_t)n * sizeof(float);
+        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), bytes, stream);
+        if (e != hipSuccess || ws == nullptr) {
+            g_last_error = std::string("hipMallocAsync of the split-K workspace: ") + hipGetErrorString(e);
+            return PAM_ERROR_ALLOC;
+        }
+    }
+    pam_status_t result = PAM_SUCCESS;
+    for (int64_t b0 = 0; b0 < batch && result == PAM_SUCCESS; b0 += gz_max) {
+        const int64_t nb = std::min(gz_max, batch - b0);
+        p.A = A + b0 * sa;
+        p.B = B + b0 * sb;
+        p.C = C + b0 * sc;
+        p.W = ws;
+        p.vec_c = ws ? (n % 4 == 0) : (aligned16(C) && ldc % 4 == 0 && (batch == 1 || sc % 4 == 0));
+        hipError_t e = pamk::launch_pam_gemm(plan.tile_m, plan.tile_n, ta == PAM_OP_T, tb == PAM_OP_T, p, nb, stream);
+        if (e != hipSuccess) {
+            result = fail_hip(e, "gemm kernel launch");
+            break;
+        }
+        if (ws) {
+            e = pamk::launch_splitk_reduce(ws, p.C, (int32_t)m, (int32_t)n, ldc, sc, plan.splits, nb, stream);
+            if (e != hipSuccess)
+                result = fail_hip(e, "split-K reduce launch");
+        }
+    }
+    if (ws) {
+        hipError_t e = hipFreeAsync(ws, stream);
+        if (e != hipSuccess && result == PAM_SUCCESS)
+            result = fail_hip(e, "hipFreeAsync of the split-K workspace");
+    }
+    return result;
+}
+
+int query_simds_per_cu(int device) {
+    // HSA agent enumeration order matches HIP device order for GPU agents.
+    struct Ctx {
+        int want, seen, simds;
+    } ctx{device, 0, 0};
+    if (hsa_init() != HSA_STATUS_SUCCESS)
+        return 0;
+    hsa_iterate_agents(
+        [](hsa_agent_t agent, void *data) -> hsa_status_t {
+            auto *c = static_cast<Ctx *>(data);
+            hsa_device_type_t type;
+            if (hsa_agent_get_info(agent, HSA_AGENT_INFO_DEVICE, &type) != HSA_STATUS_SUCCESS)
+                return HSA_STATUS_SUCCESS;
+            if (type != HSA_DEVICE_TYPE_GPU)
+                return HSA_STATUS_SUCCESS;
+            if (c->seen++ == c->want) {
+                uint32_t v = 0;
+                if (hsa_agent_get_info(agent, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_NUM_SIMDS_PER_CU, &v) ==
+                    HSA_STATUS_SUCCESS)
+                    c->simds = (int)v;
+                return HSA_STATUS_INFO_BREAK;
+            }
+            return HSA_STATUS_SUCCESS;
+        },
+        &ctx);
+    hsa_shut_down();
+    return ctx.simds;
+}
+
+}  // namespace
+
+extern "C" {
+
+pam_status_t pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream) {
+    if (n < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "n must be >= 0");
+    if (n == 0)
+        return PAM_SUCCESS;
+    if (a == nullptr || b == nullptr || out == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "a, b and out must be non-NULL");
+    pam_status_t st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    hipError_t e = pamk::launch_pam_mul(a, b, out, n, stream);
+    if (e != hipSuccess)
+        return fail_hip(e, "pam_mul kernel launch");
+    return PAM_SUCCESS;
+}
+
+pam_status_t pam_gemm(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                      const float *B, int64_t ldb, float *C, int64_t ldc, hipStream_t stream) {
+    pam_status_t st = validate(transA, transB, m, n, k, A, lda, 0, B, ldb, 0, C, ldc, 0, 1);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (m == 0 || n == 0)
+        return PAM_SUCCESS;
+    return run_gemm(transA, transB, m, n, k, A, lda, 0, B, ldb, 0, C, ldc, 0, 1, choose_plan(m, n, k, 1), stream);
+}
+
+pam_status_t pam_gemm_batched(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k, const float *A,
+                              int64_t lda, int64_t strideA, const float *B, int64_t ldb, int64_t strideB, float *C,
+                              int64_t ldc, int64_t strideC, int64_t batch, hipStream_t stream) {
+    pam_status_t st = validate(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (m == 0 || n == 0 || batch == 0)
+        return PAM_SUCCESS;
+    return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch,
+                    choose_plan(m, n, k, batch), stream);
+}
+
+pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_plan_t *plan) {
+    if (plan == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "plan is NULL");
+    if (m <= 0 || n <= 0 || k < 0 || batch <= 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n, batch must be > 0 and k >= 0");
+    const Plan p = choose_plan(m, n, std::max<int64_t>(k, 1), batch);
+    plan->tile_m = p.tile_m;
+    plan->tile_n = p.tile_n;
+    plan->splits = p.splits;
+    return PAM_SUCCESS;
+}
+
+pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                                        const float *A, int64_t lda, int64_t strideA, const float *B, int64_t ldb,
+                                        int64_t strideB, float *C, int64_t ldc, int64_t strideC, int64_t batch,
+                                        const pam_plan_t *plan, hipStream_t stream) {
+    pam_status_t st = validate(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (plan == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "plan is NULL");
+    const bool tile_ok = (plan->tile_m == 128 && plan->tile_n == 128) || (plan->tile_m == 128 && plan->tile_n == 64) ||
+                         (plan->tile_m == 64 && plan->tile_n == 64);
+    if (!tile_ok)
+        return fail(PAM_ERROR_INVALID_VALUE, "tile must be 128x128, 128x64 or 64x64");
+    if (plan->splits < 1 || plan->splits > kMaxSplits)
+        return fail(PAM_ERROR_INVALID_VALUE, "splits must be in [1, 64]");
+    if (m == 0 || n == 0 || batch == 0)
+        return PAM_SUCCESS;
+    Plan p{plan->tile_m, plan->tile_n, 1, std::max<int64_t>(k, 1)};
+    if (plan->splits > 1 && k > 0) {
+        const int64_t per = ceil_div(ceil_div(k, plan->splits), pamk::kChunkK) * pamk::kChunkK;
+        p.k_per_split = per;
+        p.splits = (int)ceil_div(k, per);
+    }
+    return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch, p, stream);
+}
+
+pam_status_t pam_device_info(int device, pam_device_info_t *info) {
+    if (info == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "info is NULL");
+    std::memset(info, 0, sizeof *info);
+    hipDeviceProp_t prop;
+    hipError_t e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess)
+        return fail_hip(e, "hipGetDeviceProperties");
+    int clock_khz = 0;
+    e = hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeClockRate, device);
+    if (e != hipSuccess)
+        return fail_hip(e, "hipDeviceGetAttribute(ClockRate)");
+    info->compute_units = prop.multiProcessorCount;
+    info->simds_per_cu = query_simds_per_cu(device);
+    info->wavefront_size = prop.warpSize;
+    // A SIMD retires one wavefront instruction every 64 / 16 clocks: 16 lanes per clock.
+    info->lanes_per_simd = 16;
+    info->clock_khz = clock_khz;
+    info->valu_lane_ops_per_s =
+        double(info->compute_units) * info->simds_per_cu * info->lanes_per_simd * double(clock_khz) * 1e3;
+    std::snprintf(info->arch, sizeof info->arch, "%s", prop.gcnArchName);
+    return PAM_SUCCESS;
+}
+
+const char *pam_status_string(pam_status_t s) {
+    switch (s) {
+    case PAM_SUCCESS:
+        return "PAM_SUCCESS";
+    case PAM_ERROR_INVALID_VALUE:
+        return "PAM_ERROR_INVALID_VALUE";
+    case PAM_ERROR_LAUNCH:
+        return "PAM_ERROR_LAUNCH";
+    case PAM_ERROR_NOT_SUPPORTED:
+        return "PAM_ERROR_NOT_SUPPORTED";
+    case PAM_ERROR_ALLOC:
+        return "PAM_ERROR_ALLOC";
+    }
+    return "PAM_ERROR_UNKNOWN";
+}
+
+const char *pam_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,44 @@
+// Internal interface between the C-ABI layer (pam_api.cpp) and the HIP
+// kernels (pam_kernels.hip).  Not installed; not part of the public ABI.
+#pragma once
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+namespace pamk {
+
+// K extent of one LDS chunk.
+constexpr int kChunkK = 16;
+
+// Arguments of one (batched, possibly split-K) PAM matrix product launch.
+struct GemmParams {
+    const float *A;
+    const float *B;
+    float *C;          // final output (used when W == nullptr)
+    float *W;          // split-K partial sums [batch][splits][m][n], or nullptr
+    int64_t lda, ldb, ldc;
+    int64_t strideA, strideB, strideC;
+    int32_t m, n, k;
+    int32_t k_per_split;  // multiple of kChunkK
+    int32_t splits;
+    int32_t tiles_n;
+    int32_t vec_a;        // float4 global loads of A are aligned
+    int32_t vec_b;        // float4 global loads of B are aligned
+    int32_t vec_c;        // float4 stores of the output are aligned
+};
+
+hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
+
+// tile_m, tile_n in {64, 128}; grid = (tiles_m * tiles_n, splits, batch_in_launch).
+hipError_t launch_pam_gemm(int tile_m, int tile_n, bool trans_a, bool trans_b,
+                           const GemmParams &p, int64_t batch, hipStream_t stream);
+
+// C[b][i][j] = sum_s W[b][s][i][j], s in increasing order.
+hipError_t launch_splitk_reduce(const float *W, float *C, int32_t m, int32_t n, int64_t ldc,
+                                int64_t strideC, int32_t splits, int64_t batch, hipStream_t stream);
+
+// C[b][i][j] = +0.0f for a k == 0 product.
+hipError_t launch_fill_zero(float *C, int32_t m, int32_t n, int64_t ldc, int64_t strideC,
+                            int64_t batch, hipStream_t stream);
+
+}  // namespace pamk

@@ -1,0 +1,102 @@
+"""The C-ABI library on the host: it loads, exports every declared symbol and
+rejects bad arguments before touching the GPU.  No compute calls."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2305_17190_amd as pam
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "pam.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pam_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pam.library_path()):
+        pytest.skip("libpam.so not built (run __graft_entry__.build())")
+    return pam.load()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ("pam_mul", "pam_gemm", "pam_gemm_batched", "pam_status_string", "pam_last_error"):
+        assert want in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} declared in pam.h but not exported"
+    assert set(pam.EXPORTS) == set(declared_functions())
+
+
+def test_status_strings(lib):
+    assert lib.pam_status_string(0) == b"PAM_SUCCESS"
+    assert lib.pam_status_string(1) == b"PAM_ERROR_INVALID_VALUE"
+    assert lib.pam_status_string(4) == b"PAM_ERROR_ALLOC"
+
+
+def gemm_call(lib, **kw):
+    a = dict(ta=0, tb=0, m=4, n=4, k=4, A=8, lda=4, B=8, ldb=4, C=8, ldc=4)
+    a.update(kw)
+    return lib.pam_gemm(a["ta"], a["tb"], a["m"], a["n"], a["k"], a["A"], a["lda"], a["B"], a["ldb"],
+                        a["C"], a["ldc"], None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(m=-1), dict(n=-2), dict(k=-3), dict(ta=2), dict(tb=7),
+    dict(lda=3), dict(ldb=3), dict(ldc=3), dict(ta=1, lda=3, m=4),
+    dict(A=None), dict(B=None), dict(C=None), dict(m=1 << 31),
+])
+def test_gemm_rejects_bad_arguments(lib, kw):
+    assert gemm_call(lib, **kw) == 1
+    assert lib.pam_last_error() != b""
+
+
+def test_batched_rejects_negative_stride_and_batch(lib):
+    i = lib.pam_gemm_batched(0, 0, 4, 4, 4, 8, 4, -1, 8, 4, 16, 8, 4, 16, 2, None)
+    assert i == 1
+    assert lib.pam_gemm_batched(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, -1, None) == 1
+
+
+def test_empty_products_launch_nothing(lib):
+    # m == 0 / n == 0 / batch == 0 succeed without any device work or pointers.
+    assert gemm_call(lib, m=0, A=None, C=None, lda=4) == 0
+    assert gemm_call(lib, n=0, B=None, C=None, ldb=1, ldc=1) == 0
+    assert lib.pam_gemm_batched(0, 0, 4, 4, 4, None, 4, 0, None, 4, 0, None, 4, 0, 0, None) == 0
+    assert lib.pam_mul(None, None, None, 0, None) == 0
+    assert lib.pam_mul(None, None, None, -1, None) == 1
+
+
+def test_plan_selection_is_host_logic(lib):
+    # Large square products use the 128x128 tile without split-K.
+    assert pam.plan(16384, 4096, 4096) == (128, 128, 1)
+    # Small output, long K: split-K.
+    tm, tn, s = pam.plan(768, 192, 12608)
+    assert s > 1 and (tm, tn) in ((128, 64), (64, 64), (128, 128))
+    # Ragged n = 192 avoids a 128-wide tile (33% padding).
+    assert pam.plan(12608, 192, 768)[1] == 64
+    with pytest.raises(pam.PamError):
+        pam.plan(0, 4, 4)
+
+
+def test_with_plan_rejects_bad_tiles(lib):
+    P = pam._Plan(96, 64, 1)
+    assert lib.pam_gemm_batched_with_plan(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1, ctypes.byref(P), None) == 1
+    P = pam._Plan(128, 128, 0)
+    assert lib.pam_gemm_batched_with_plan(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1, ctypes.byref(P), None) == 1
+
+
+def test_binding_refuses_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    a = torch.ones(8)
+    with pytest.raises(pam.PamError):
+        pam.mul(a, a)
+    with pytest.raises(pam.PamError):
+        pam.gemm(torch.ones(2, 2), torch.ones(2, 2))

@@ -1,0 +1,179 @@
+"""PAM matrix products on the GPU against the CPU oracle, element by element.
+
+Sizes span several tiles with ragged tails in every dimension.  The data
+kinds drive each LDS encoding of the kernel: normal values (FAST), zeros,
+denormals and underflowing products (GENERIC), and inf / NaN / |x| >= 2^64
+(SPECIAL).  Every tiling and split-K setting is exercised through the
+explicit-plan entry point.
+"""
+import numpy as np
+import pytest
+
+import paper_2305_17190_amd as pam
+from gpu_util import check_gemm, device, note, oracle_gemm, to_dev
+from oracle import pam_ref
+
+pytestmark = pytest.mark.gpu
+
+PLANS = [(128, 128, 1), (128, 64, 1), (64, 64, 1), (128, 128, 3), (128, 64, 7), (64, 64, 2)]
+TRANS = [(False, False), (False, True), (True, False), (True, True)]
+
+
+def make(kind: str, shape, seed: int) -> np.ndarray:
+    g = np.random.default_rng(seed)
+    x = g.standard_normal(shape).astype(np.float32)
+    flat = x.reshape(-1)
+    n = flat.size
+    if kind == "normal":
+        return x
+    if kind == "zeros_tiny":
+        idx = g.choice(n, size=max(1, n // 25), replace=False)
+        third = len(idx) // 3
+        flat[idx[:third]] = np.where(g.random(third) < 0.5, 0.0, -0.0)
+        flat[idx[third:2 * third]] = (g.uniform(0.5, 2.0, len(idx[third:2 * third])) * 2.0 ** -126).astype(np.float32)
+        flat[idx[2 * third:]] = np.float32(3e-41)                       # denormal
+        return x
+    if kind == "underflow":
+        e = g.integers(-75, -50, size=n)
+        return (np.sign(flat) * np.ldexp(1.0 + np.abs(flat) % 1.0, e)).astype(np.float32).reshape(shape)
+    if kind == "wide":
+        e = g.integers(-70, 55, size=n)
+        return (np.sign(flat) * np.ldexp(1.0 + np.abs(flat) % 1.0, e)).astype(np.float32).reshape(shape)
+    if kind == "specials":
+        idx = g.choice(n, size=max(3, n // 200), replace=False)
+        vals = np.array([np.inf, -np.inf, np.nan, 2.0 ** 70, -(2.0 ** 65), 0.0], dtype=np.float32)
+        flat[idx] = vals[g.integers(0, len(vals), size=len(idx))]
+        return x
+    raise ValueError(kind)
+
+
+def run_case(m, n, k, ta, tb, kind_a, kind_b, plan=None, pad=(0, 0, 0), seed=0, batch=1):
+    """Build op(A), op(B) with optional leading-dimension padding and compare."""
+    a_rows, a_cols = (k, m) if ta else (m, k)
+    b_rows, b_cols = (n, k) if tb else (k, n)
+    a_buf = make(kind_a, (batch, a_rows, a_cols + pad[0]), seed)
+    b_buf = make(kind_b, (batch, b_rows, b_cols + pad[1]), seed + 1)
+    lda, ldb = a_cols + pad[0], b_cols + pad[1]
+    ldc = n + pad[2]
+    note(f"gemm m={m} n={n} k={k} ta={ta} tb={tb} A={kind_a} B={kind_b} plan={plan} pad={pad} batch={batch}")
+    da = to_dev(a_buf)[:, :, :a_cols]
+    db = to_dev(b_buf)[:, :, :b_cols]
+    import torch
+    c_full = torch.full((batch, m, ldc), float("nan"), device=device())
+    c = c_full[:, :, :n]
+    pam.bmm(da, db, trans_a=ta, trans_b=tb, out=c, plan=plan)
+    got = c_full.cpu().numpy()
+    if pad[2]:
+        assert np.all(np.isnan(got[:, :, n:])), "wrote outside the output's columns"
+    c_ref, s_ref = oracle_gemm(a_buf, b_buf, ta, tb, m, n, k, lda, ldb, a_buf[0].size, b_buf[0].size,
+                               batches=list(range(batch)))
+    check_gemm(got[:, :, :n], c_ref, s_ref, k, f"m={m} n={n} k={k} ta={ta} tb={tb} {kind_a}/{kind_b} {plan}")
+
+
+@pytest.mark.parametrize("plan", PLANS, ids=lambda p: "x".join(map(str, p)))
+@pytest.mark.parametrize("ta,tb", TRANS, ids=["NN", "NT", "TN", "TT"])
+def test_plans_and_layouts_normal(plan, ta, tb):
+    run_case(203, 150, 333, ta, tb, "normal", "normal", plan=plan, seed=11)
+
+
+@pytest.mark.parametrize("ta,tb", TRANS, ids=["NN", "NT", "TN", "TT"])
+@pytest.mark.parametrize("kinds", [("zeros_tiny", "normal"), ("normal", "zeros_tiny"), ("underflow", "underflow"),
+                                   ("wide", "wide"), ("specials", "normal"), ("normal", "specials"),
+                                   ("zeros_tiny", "specials")], ids=lambda k: "-".join(k))
+def test_encodings(kinds, ta, tb):
+    run_case(130, 200, 100, ta, tb, kinds[0], kinds[1], plan=(128, 64, 2), seed=21)
+
+
+@pytest.mark.parametrize("pad", [(4, 4, 4), (1, 3, 5), (0, 0, 1)])
+@pytest.mark.parametrize("ta,tb", TRANS, ids=["NN", "NT", "TN", "TT"])
+def test_leading_dimension_padding(pad, ta, tb):
+    run_case(77, 91, 64, ta, tb, "normal", "zeros_tiny", pad=pad, seed=31)
+
+
+@pytest.mark.parametrize("mnk", [(1, 1, 1), (1, 300, 17), (300, 1, 17), (64, 64, 16), (129, 129, 1), (5, 7, 3),
+                                 (256, 256, 4096), (16, 16, 2000)])
+def test_shapes(mnk):
+    m, n, k = mnk
+    run_case(m, n, k, False, True, "normal", "normal", seed=41)
+
+
+@pytest.mark.parametrize("ta,tb", TRANS, ids=["NN", "NT", "TN", "TT"])
+def test_batched_strides(ta, tb):
+    run_case(70, 40, 50, ta, tb, "normal", "zeros_tiny", batch=5, seed=51)
+
+
+def test_batched_auto_plan_split():
+    run_case(96, 64, 512, False, False, "normal", "normal", batch=3, seed=52)
+
+
+def test_batched_broadcast_stride_zero():
+    import torch
+    note("bmm with a stride-0 (broadcast) B")
+    g = np.random.default_rng(61)
+    a = g.standard_normal((4, 33, 21)).astype(np.float32)
+    b = g.standard_normal((21, 19)).astype(np.float32)
+    db = to_dev(b).unsqueeze(0).expand(4, 21, 19)
+    c = pam.bmm(to_dev(a), db).cpu().numpy()
+    for z in range(4):
+        c_ref, s_ref = pam_ref.pam_gemm_ref(a[z], b)
+        check_gemm(c[z], c_ref, s_ref, 21, f"broadcast z={z}")
+
+
+def test_identity_is_exact():
+    note("gemm with B = I")
+    g = np.random.default_rng(71)
+    a = g.standard_normal((150, 140)).astype(np.float32)
+    eye = np.eye(140, dtype=np.float32)
+    for plan in PLANS:
+        c = pam.bmm(to_dev(a[None]), to_dev(eye[None]), plan=plan).cpu().numpy()[0]
+        assert np.array_equal(c.view(np.uint32), a.view(np.uint32)), f"identity not exact with plan {plan}"
+
+
+def test_k1_equals_elementwise():
+    note("gemm K = 1 equals broadcast pam_mul")
+    g = np.random.default_rng(72)
+    col = g.standard_normal((90, 1)).astype(np.float32)
+    row = g.standard_normal((1, 70)).astype(np.float32)
+    row[0, 3] = 0.0
+    c = pam.gemm(to_dev(col), to_dev(row)).cpu().numpy()
+    want = pam_ref.pam_mul_ref(np.repeat(col, 70, 1), np.repeat(row, 90, 0))
+    assert np.array_equal(c, want)
+
+
+def test_k0_writes_zeros():
+    import torch
+    note("gemm K = 0")
+    a = torch.empty((7, 0), device=device())
+    b = torch.empty((0, 9), device=device())
+    c = torch.full((7, 9), 5.0, device=device())
+    pam.gemm(a, b, out=c)
+    assert torch.all(c == 0)
+
+
+def test_deterministic():
+    import torch
+    note("gemm bitwise repeatable, split-K plan")
+    g = np.random.default_rng(73)
+    a = to_dev(g.standard_normal((1, 200, 900)).astype(np.float32))
+    b = to_dev(g.standard_normal((1, 900, 120)).astype(np.float32))
+    c1 = pam.bmm(a, b, plan=(64, 64, 6))
+    c2 = pam.bmm(a, b, plan=(64, 64, 6))
+    assert torch.equal(c1.view(torch.int32), c2.view(torch.int32))
+
+
+def test_linear_layer_forms_with_torch_views():
+    """Forward and both approximate-derivative products of one linear layer."""
+    import torch
+    note("linear layer fwd / dX / dW through pam.gemm")
+    g = np.random.default_rng(74)
+    x = g.standard_normal((257, 96)).astype(np.float32)
+    w = (0.05 * g.standard_normal((130, 96))).astype(np.float32)
+    dy = (1e-3 * g.standard_normal((257, 130))).astype(np.float32)
+    dx_, dw_, ddy = to_dev(x), to_dev(w), to_dev(dy)
+    y = pam.gemm(dx_, dw_, trans_b=True).cpu().numpy()
+    dX = pam.gemm(ddy, dw_).cpu().numpy()
+    dW = pam.gemm(ddy, dx_, trans_a=True).cpu().numpy()
+    for got, (a, b, ta, tb), k in ((y, (x, w, False, True), 96), (dX, (dy, w, False, False), 130),
+                                   (dW, (dy, x, True, False), 257)):
+        c_ref, s_ref = pam_ref.pam_gemm_ref(a, b, ta, tb)
+        check_gemm(got, c_ref, s_ref, k, f"linear ta={ta} tb={tb}")

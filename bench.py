@@ -112,6 +112,8 @@ def main() -> int:
     ap.add_argument("--workload", default="w5", choices=["w1", "w2", "w3", "w4", "w5"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy (reference kernel for HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -129,6 +131,14 @@ def main() -> int:
         return 1
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copied 3 x {src.numel() * 4} bytes")
+        return 0
     pam.load()
 
     wid = int(args.workload[1:])

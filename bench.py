@@ -28,8 +28,10 @@ sys.path.insert(0, ROOT)
 # the two encodings (one operand pre-biased once per LDS chunk) and one
 # float32 add.
 ALGO_LANE_OPS_PER_MAC = 2
-# MI355X nominal: 256 CUs x 4 SIMDs x 16 lanes per clock x 2.4 GHz.
-NOMINAL_VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
+# MI355X nominal: 256 CUs x 4 SIMDs x 32 lanes per clock x 2.4 GHz for the
+# full-rate ops (int32 add, float32 add/mul/fma) = the 157.3 TFLOP/s
+# float32-vector figure counted as one lane op per fma.
+NOMINAL_VALU_LANE_OPS = 256 * 4 * 32 * 2.4e9
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2305_17190_amd", "csrc", "pam_kernels.hip")
 
 

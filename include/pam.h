@@ -128,8 +128,10 @@ pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB,
 
 /*
  * Figures of `device` that set the vector-ALU roofline: compute units,
- * SIMDs per compute unit, lanes each SIMD retires per clock, peak engine
- * clock (kHz) and wavefront size, read from the HIP runtime and HSA.
+ * SIMDs per compute unit and peak engine clock (kHz) read from the HIP
+ * runtime and HSA, wavefront size, and the lanes a SIMD retires per clock
+ * for the full-rate ops of the PAM matrix product (int32 add, float32 add,
+ * mul and fma: 32 on gfx950; other vector ops retire 16).
  * valu_lane_ops_per_s = cus * simds_per_cu * lanes_per_simd * clock.
  */
 typedef struct {

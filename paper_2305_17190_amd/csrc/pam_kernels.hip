@@ -10,35 +10,35 @@
 // The matrix product is a vector-ALU contraction (PAM is not a product, so
 // the matrix cores do not apply).  Each workgroup owns a BM x BN output tile,
 // each thread an 8 x 8 register micro-tile, and K advances in chunks of 16
-// staged through LDS.  When a chunk is written to LDS its operands are
-// re-encoded once so that the per-MAC work is as small as the chunk's values
-// allow; the workgroup votes on which encoding a chunk gets:
+// staged through LDS.  On gfx950 the integer add and the float32 add, mul and
+// fma issue at twice the rate of other vector ops (max, add3, saturating
+// add), so the per-MAC work is built from those four only.
 //
-//   FAST     every operand has exponent field in [64, 190], so no product
-//            can leave the normal range.  LDS holds a's encoding and b's
-//            encoding minus the bias; per MAC: one v_add_u32 (the sign
-//            bits add mod 2^32 to their exclusive or) + one v_add_f32.
-//   GENERIC  every operand is finite with |x| < 2^64 (zeros, denormals and
-//            products that underflow allowed).  Magnitudes are shifted into
-//            a domain where one signed-saturating add clamps every underflow
-//            (and every zero/denormal operand, encoded as INT32_MIN) to
-//            INT32_MIN, i.e. to magnitude 0; per MAC: v_add_i32 clamp +
-//            v_add3_u32 (restores the offset and adds both sign words) +
-//            v_add_f32.  Results in (0, 2^-126) come out as denormal
-//            encodings; the kernels run with float32 denormals flushed, so
-//            the accumulate treats them as the zero PAM defines.
-//   SPECIAL  anything else (inf, NaN, |x| >= 2^64): raw encodings and the
-//            complete per-MAC definition.  Never taken on finite data whose
-//            magnitudes stay below 2^64.
+// SCALED encoding (written to LDS once per chunk):
+//   A element a = (-1)^s 2^E (1 + M):  aM = encoding of 1 + M (exponent
+//       field 127, a's mantissa) and m = a with its mantissa cleared, i.e.
+//       the float +-2^E, or +-0 when a is zero/denormal.
+//   B element b:  b' = encoding of b minus 0x3F800000 (zero and denormal b
+//       are encoded as a signed zero first).
+//   Then t = aM + b' (one int add) is the encoding of PAM(1 + M, b): adding
+//   1 + M's mantissa to b's encoding is Sec. 2.2's sum with E = 0 on the A
+//   side.  PAM is exact under power-of-two scaling (Fig. 2: the pattern
+//   repeats per octave), so t * m = PAM(a, b) whenever the result is a normal
+//   number; the float multiply also supplies the sign.  A zero b makes t a
+//   denormal encoding, which the float unit (denormals flushed) reads as 0.
 //
-// Encodings used by GENERIC (m = |x| encoding, valid m in [2^23, 0x5F7FFFFF]):
-//   x_A = m_A - 0x5F7FFFFF            in [-0x5EFFFFFF, 0], or INT32_MIN
-//   y_B = m_B - 0x3F800000 - 0x20800001 in [-0x5F800001, -0x00800002], or INT32_MIN
-//   sat(x_A + y_B) = sat(R - 2^31),    R = m_A + m_B - 0x3F800000
-// R >= 0 gives the PAM magnitude R + (-2^31) exactly; R < 0 (underflow)
-// saturates.  Since x_A <= 0 and y_B < 0, a zero/denormal operand on either
-// side also lands on INT32_MIN.  R <= 0x7F7FFFFE, so nothing overflows.
-// Adding (sign_A ^ 2^31) + sign_B mod 2^32 then yields sign | magnitude.
+//   S2 (per MAC: v_add_u32, v_fmac_f32): acc = fma(t, m, acc).  Exact when
+//      no product underflows, which holds when every nonzero operand has
+//      exponent field in [64, 190].
+//   S3 (per MAC: v_add_u32, v_mul_f32, v_add_f32): p = t * m is rounded on
+//      its own, so an underflowing product flushes to the signed zero PAM
+//      defines; exact for all finite operands with |x| < 2^64.
+//   Each wave picks S2 or S3 per k step from a bit mask of the operands it
+//   will read at that k ("tiny": nonzero with exponent field 1..63).
+//
+// SPECIAL: a chunk holding inf, NaN or |x| >= 2^64 is written raw and
+// evaluated with the complete per-MAC definition (never taken on finite data
+// whose magnitudes stay below 2^64).
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -58,12 +58,10 @@ constexpr uint32_t kInf = 0x7F800000u;
 constexpr uint32_t kQNaN = 0x7FC00000u;
 constexpr uint32_t kExpMask = 0x7F800000u;
 
-// GENERIC-encoding offsets (see the header comment).
-constexpr uint32_t kOffA = 0x5F7FFFFFu;
-constexpr uint32_t kOffB = 0x60000001u;     // bias + 0x20800001
-constexpr int32_t kSentinel = INT32_MIN;
+constexpr uint32_t kSignExp = 0xFF800000u;
+constexpr uint32_t kMant = 0x007FFFFFu;
 
-enum : int { kFast = 0, kGeneric = 1, kSpecial = 2 };
+enum : int { kScaled = 0, kSpecial = 1 };
 
 // Complete PAM of two float32 encodings, every input class.
 __device__ __forceinline__ uint32_t pam_full(uint32_t ua, uint32_t ub) {
@@ -202,68 +200,99 @@ struct TileLoader {
         }
     }
 
-    // bit 0: some operand is outside the FAST range; bit 1: outside GENERIC.
-    __device__ __forceinline__ uint32_t classify() const {
-        uint32_t not_fast = 0, not_generic = 0;
+    // Nonzero when some element needs the SPECIAL path: inf, NaN or |x| >= 2^64.
+    __device__ __forceinline__ uint32_t needs_special() const {
+        uint32_t any = 0;
 #pragma unroll
         for (int r = 0; r < L; ++r) {
             const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
 #pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                not_fast |= ((e[c] & kExpMask) - 0x20000000u) > 0x3F000000u;   // field not in [64, 190]
-                not_generic |= (e[c] & kMag) >= 0x5F800000u;                   // |x| >= 2^64, inf, NaN
-            }
+            for (int c = 0; c < 4; ++c)
+                any |= (e[c] & kMag) >= 0x5F800000u;
         }
-        return not_fast | (not_generic << 1);
+        return any;
     }
 
-    __device__ __forceinline__ static void encode(int mode, bool is_b, uint32_t u, uint32_t &p0, uint32_t &p1) {
-        if (mode == kFast) {
-            p0 = is_b ? u - kBias : u;
-            p1 = 0u;
-        } else if (mode == kGeneric) {
-            const bool zero = (u & kExpMask) == 0u;
-            const uint32_t m = u & kMag;
-            p0 = zero ? (uint32_t)kSentinel : m - (is_b ? kOffB : kOffA);
-            p1 = is_b ? (u & kSign) : ((u & kSign) ^ kSign);
-        } else {
-            p0 = u;
-            p1 = 0u;
-        }
+    // "Tiny": a normal number with exponent field 1..63, whose products can
+    // underflow.  Zeros and denormals are not tiny (their products are exact
+    // zeros in both S2 and S3).
+    __device__ __forceinline__ static bool tiny(uint32_t u) {
+        return (u & kExpMask) - kMinNormal < (63u << 23);
     }
 
-    // Write the chunk into LDS, k-major: s[plane][kk][o].
-    template <int LDS_LD>
-    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], int mode, bool is_b, int tid) const {
+    // Write the chunk into LDS, k-major: s[plane][kk][o].  SCALED: A gets
+    // plane 0 = aM, plane 1 = m; B gets plane 0 = b'.  SPECIAL: raw words in
+    // plane 0.  Tiny elements set bit kk of mask[w] (A: the wave that reads
+    // row o, from row_wave; B: mask[b_slot], read by every wave).
+    template <int LDS_LD, typename RowWave>
+    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], int mode, bool is_b, int tid, uint32_t *mask,
+                                          int b_slot, RowWave row_wave) const {
 #pragma unroll
         for (int r = 0; r < L; ++r) {
             const int f = tid + NT * r;
             const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
             uint32_t p0[4], p1[4];
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-                encode(mode, is_b, e[c], p0[c], p1[c]);
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t u = e[c];
+                if (mode == kSpecial) {
+                    p0[c] = u;
+                    p1[c] = 0u;
+                } else if (is_b) {
+                    const uint32_t z = ((u & kExpMask) == 0u) ? (u & kSign) : u;   // denormal -> signed zero
+                    p0[c] = z - kBias;
+                    p1[c] = 0u;
+                } else {
+                    p0[c] = (u & kMant) | kBias;
+                    p1[c] = u & kSignExp;
+                }
+            }
+            int o, kk0;
             if (KCONTIG) {
-                const int o = f / (BK / 4);
-                const int kq = (f % (BK / 4)) * 4;
+                o = f / (BK / 4);
+                kk0 = (f % (BK / 4)) * 4;
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
-                    s[0][kq + c][o] = p0[c];
-                if (mode == kGeneric) {
+                    s[0][kk0 + c][o] = p0[c];
+                if (!is_b && mode != kSpecial) {
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
-                        s[1][kq + c][o] = p1[c];
+                        s[1][kk0 + c][o] = p1[c];
                 }
             } else {
-                const int kk = f / (D / 4);
-                const int oq = (f % (D / 4)) * 4;
-                *reinterpret_cast<uint4 *>(&s[0][kk][oq]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
-                if (mode == kGeneric)
-                    *reinterpret_cast<uint4 *>(&s[1][kk][oq]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
+                kk0 = f / (D / 4);
+                o = (f % (D / 4)) * 4;
+                *reinterpret_cast<uint4 *>(&s[0][kk0][o]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
+                if (!is_b && mode != kSpecial)
+                    *reinterpret_cast<uint4 *>(&s[1][kk0][o]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
+            }
+            if (mode != kSpecial) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    if (tiny(e[c])) {
+                        const int kk = KCONTIG ? kk0 + c : kk0;
+                        const int oc = KCONTIG ? o : o + c;
+                        atomicOr(&mask[is_b ? b_slot : row_wave(oc)], 1u << kk);
+                    }
+                }
             }
         }
     }
 };
+
+// S3 update of a micro-tile: the product t * m is rounded (denormal results
+// flushed) before it is added, never fused into an fma.
+__device__ __forceinline__ void s3_accumulate(float (&acc)[8][8], const uint32_t (&am)[8], const uint32_t (&mm)[8],
+                                              const uint32_t (&bb)[8]) {
+#pragma clang fp contract(off)
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float prod = __uint_as_float(am[i] + bb[j]) * __uint_as_float(mm[i]);
+            acc[i][j] = acc[i][j] + prod;
+        }
+}
 
 template <int LD>
 __device__ __forceinline__ void lds_frag(const uint32_t (*s)[kChunkK][LD], int plane, int kk, int i0, int half,
@@ -280,18 +309,21 @@ __global__ void __launch_bounds__(BM * BN / 64) pam_gemm_kernel(GemmParams p) {
     constexpr int NT = BM * BN / 64;
     constexpr int NW = NT / 64;
     constexpr int TXN = BN / 8;            // threads along n
+    constexpr int TY_PER_WAVE = 64 / TXN;  // micro-tile rows (of 2 x 4) per wave
     constexpr int HM = BM / 2;
     constexpr int HN = BN / 2;
     constexpr int LDA = BM + 4;            // padded LDS rows, 16-byte aligned
     constexpr int LDB = BN + 4;
 
-    __shared__ uint32_t sA[2][BK][LDA];    // plane 0: value word, plane 1: sign word (GENERIC)
-    __shared__ uint32_t sB[2][BK][LDB];
+    __shared__ uint32_t sA[2][BK][LDA];    // SCALED: plane 0 aM, plane 1 m; SPECIAL: plane 0 raw
+    __shared__ uint32_t sB[1][BK][LDB];    // SCALED: b'; SPECIAL: raw
     __shared__ uint32_t sVote[NW];
+    __shared__ uint32_t sMask[2][NW + 1];  // per chunk parity: tiny bits per wave (A rows) and for B
 
     const int tid = threadIdx.x;
     const int tx = tid % TXN;
     const int ty = tid / TXN;
+    const int wave = tid >> 6;
     const int tm = blockIdx.x / p.tiles_n;
     const int tn = blockIdx.x % p.tiles_n;
     const int m0 = tm * BM;
@@ -306,6 +338,7 @@ __global__ void __launch_bounds__(BM * BN / 64) pam_gemm_kernel(GemmParams p) {
 
     TileLoader<BM, NT, !TA> la;
     TileLoader<BN, NT, TB> lb;
+    auto row_wave = [](int o) { return ((o % HM) / 4) / TY_PER_WAVE; };
 
     float acc[8][8];
 #pragma unroll
@@ -314,27 +347,31 @@ __global__ void __launch_bounds__(BM * BN / 64) pam_gemm_kernel(GemmParams p) {
         for (int j = 0; j < 8; ++j)
             acc[i][j] = 0.0f;
 
+    if (tid < 2 * (NW + 1))
+        (&sMask[0][0])[tid] = 0u;
+
     if (nchunks > 0) {
         la.load(A, p.lda, m0, p.m, kb, ke, p.vec_a != 0, tid);
         lb.load(B, p.ldb, n0, p.n, kb, ke, p.vec_b != 0, tid);
     }
 
     for (int c = 0; c < nchunks; ++c) {
-        // Workgroup vote on the chunk's encoding.
-        const uint32_t f = la.classify() | lb.classify();
-        const uint64_t nf = __ballot(f & 1u);
-        const uint64_t ng = __ballot(f & 2u);
+        // Workgroup vote: SPECIAL if any operand of the chunk is inf, NaN or >= 2^64.
+        const uint64_t sp = __ballot(la.needs_special() | lb.needs_special());
         if ((tid & 63) == 0)
-            sVote[tid >> 6] = (nf ? 1u : 0u) | (ng ? 2u : 0u);
+            sVote[wave] = sp ? 1u : 0u;
         __syncthreads();
         uint32_t v = 0;
 #pragma unroll
         for (int w = 0; w < NW; ++w)
             v |= sVote[w];
-        const int mode = (v & 2u) ? kSpecial : ((v & 1u) ? kGeneric : kFast);
+        const int mode = v ? kSpecial : kScaled;
 
-        la.template store<LDA>(sA, mode, false, tid);
-        lb.template store<LDB>(sB, mode, true, tid);
+        uint32_t *mask = sMask[c & 1];
+        if (tid < NW + 1)
+            sMask[(c + 1) & 1][tid] = 0u;   // next chunk's masks; last read two chunks ago
+        la.template store<LDA>(sA, mode, false, tid, mask, NW, row_wave);
+        lb.template store<LDB>(sB, mode, true, tid, mask, NW, row_wave);
         __syncthreads();
 
         if (c + 1 < nchunks) {
@@ -343,33 +380,37 @@ __global__ void __launch_bounds__(BM * BN / 64) pam_gemm_kernel(GemmParams p) {
             lb.load(B, p.ldb, n0, p.n, k0, ke, p.vec_b != 0, tid);
         }
 
-        if (mode == kFast) {
-#pragma unroll
-            for (int kk = 0; kk < BK; ++kk) {
-                uint32_t a[8], b[8];
-                lds_frag<LDA>(sA, 0, kk, ty * 4, HM, a);
-                lds_frag<LDB>(sB, 0, kk, tx * 4, HN, b);
+        if (mode == kScaled) {
+            // Accumulation order is free, so a wave runs its S2 k steps first
+            // and its S3 k steps after them; neither loop body branches.
+            const uint32_t slow = __builtin_amdgcn_readfirstlane(mask[wave] | mask[NW]) & 0xFFFFu;
+            auto s2_step = [&](int kk) {
+                uint32_t am[8], mm[8], bb[8];
+                lds_frag<LDA>(sA, 0, kk, ty * 4, HM, am);
+                lds_frag<LDA>(sA, 1, kk, ty * 4, HM, mm);
+                lds_frag<LDB>(sB, 0, kk, tx * 4, HN, bb);
 #pragma unroll
                 for (int i = 0; i < 8; ++i)
 #pragma unroll
                     for (int j = 0; j < 8; ++j)
-                        acc[i][j] += __uint_as_float(a[i] + b[j]);
-            }
-        } else if (mode == kGeneric) {
+                        acc[i][j] = __builtin_fmaf(__uint_as_float(am[i] + bb[j]), __uint_as_float(mm[i]), acc[i][j]);
+            };
+            if (slow == 0u) {
 #pragma unroll
-            for (int kk = 0; kk < BK; ++kk) {
-                uint32_t x[8], sa[8], y[8], sb[8];
-                lds_frag<LDA>(sA, 0, kk, ty * 4, HM, x);
-                lds_frag<LDA>(sA, 1, kk, ty * 4, HM, sa);
-                lds_frag<LDB>(sB, 0, kk, tx * 4, HN, y);
-                lds_frag<LDB>(sB, 1, kk, tx * 4, HN, sb);
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const int32_t t = __builtin_elementwise_add_sat((int32_t)x[i], (int32_t)y[j]);
-                        acc[i][j] += __uint_as_float((uint32_t)t + sa[i] + sb[j]);
-                    }
+                for (int kk = 0; kk < BK; ++kk)
+                    s2_step(kk);
+            } else {
+                for (uint32_t todo = ~slow & 0xFFFFu; todo != 0u; todo &= todo - 1u)
+                    s2_step(__builtin_ctz(todo));
+                for (uint32_t todo = slow; todo != 0u; todo &= todo - 1u) {
+                    // S3: the product is rounded (and flushed) before the add.
+                    const int kk = __builtin_ctz(todo);
+                    uint32_t am[8], mm[8], bb[8];
+                    lds_frag<LDA>(sA, 0, kk, ty * 4, HM, am);
+                    lds_frag<LDA>(sA, 1, kk, ty * 4, HM, mm);
+                    lds_frag<LDB>(sB, 0, kk, tx * 4, HN, bb);
+                    s3_accumulate(acc, am, mm, bb);
+                }
             }
         } else {
 #pragma unroll 1

@@ -177,3 +177,52 @@ def test_linear_layer_forms_with_torch_views():
                                    (dW, (dy, x, True, False), 257)):
         c_ref, s_ref = pam_ref.pam_gemm_ref(a, b, ta, tb)
         check_gemm(got, c_ref, s_ref, k, f"linear ta={ta} tb={tb}")
+
+
+def pow2_operands(shape, seed, decoy_frac):
+    """Signed powers of two 2^-57..2^-55, 5% zeros, some denormals, and
+    'decoys' +-2^-72 (exponent field 55) whose products with every other
+    operand underflow (below 2^-126) and must add exactly nothing."""
+    g = np.random.default_rng(seed)
+    e = g.integers(-57, -54, size=shape)
+    x = (np.where(g.random(shape) < 0.5, 1.0, -1.0) * np.ldexp(1.0, e)).astype(np.float32)
+    r = g.random(shape)
+    x[r < 0.05] = 0.0
+    x[(r >= 0.05) & (r < 0.06)] = np.float32(1e-40)
+    x[(r >= 0.06) & (r < 0.06 + decoy_frac)] = np.float32(-(2.0 ** -72))
+    return x
+
+
+@pytest.mark.parametrize("decoys", [(0.0, 0.0), (0.01, 0.0), (0.0, 0.01), (0.02, 0.02), (0.3, 0.3)],
+                         ids=["none", "A", "B", "both", "dense"])
+@pytest.mark.parametrize("plan", [(128, 128, 1), (128, 64, 2), (64, 64, 1)], ids=lambda p: "x".join(map(str, p)))
+@pytest.mark.parametrize("ta,tb", [(False, True), (True, False)], ids=["NT", "TN"])
+def test_exact_sums_underflowing_products_add_nothing(decoys, plan, ta, tb):
+    """Every non-underflowing term is +-2^-114..2^-110 and the K = 300 sums
+    need at most 13 bits, so any summation order is exact in float32: the
+    result must equal the oracle bit for bit.  A product that underflows
+    (below 2^-126) is zero by definition; adding anything for it would show."""
+    m, n, k = 150, 140, 300
+    note(f"exact pow2 sums decoys={decoys} plan={plan} ta={ta} tb={tb}")
+    a_op = pow2_operands((m, k), 81, decoys[0])
+    b_op = pow2_operands((k, n), 82, decoys[1])
+    a = np.ascontiguousarray(a_op.T) if ta else a_op
+    b = np.ascontiguousarray(b_op.T) if tb else b_op
+    got = pam.bmm(to_dev(a[None]), to_dev(b[None]), trans_a=ta, trans_b=tb, plan=plan).cpu().numpy()[0]
+    c_ref, _ = pam_ref.pam_gemm_ref(a, b, ta, tb)
+    want = c_ref.astype(np.float32)
+    assert np.array_equal(want.astype(np.float64), c_ref), "test data does not give exact float32 sums"
+    bad = np.nonzero(got.view(np.uint32) != want.view(np.uint32))
+    assert bad[0].size == 0, (f"{bad[0].size} outputs differ; first ({bad[0][0]}, {bad[1][0]}): "
+                              f"got {got[bad][0]!r} want {want[bad][0]!r}")
+
+
+def test_underflow_to_exact_zero_k1():
+    """K = 1: products in the denormal range must come back as exact zeros."""
+    note("K = 1 underflowing products")
+    col = np.array([[2.0 ** -70], [1.5 * 2.0 ** -64], [-(2.0 ** -63)], [3.0]], dtype=np.float32)
+    row = np.array([[2.0 ** -60, 1.25 * 2.0 ** -63, 2.0 ** -63, -(2.0 ** -100), 0.0]], dtype=np.float32)
+    c = pam.gemm(to_dev(col), to_dev(row)).cpu().numpy()
+    want = pam_ref.pam_mul_ref(np.repeat(col, 5, 1), np.repeat(row, 4, 0))
+    assert np.array_equal(c, want), (c, want)
+    assert np.all((c == 0) | (np.abs(c) >= 2.0 ** -126)), "a denormal value reached the output"

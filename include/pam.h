@@ -78,10 +78,11 @@ pam_status_t pam_mul(const float *a, const float *b, float *out, int64_t n, hipS
  * for 0 <= i < m, 0 <= j < n, float32 accumulation.
  * The forward pass of a linear layer Y = X W^T is (N, T); its approximate
  * backward products (Table 1) are dX = dY W (N, N) and dW = dY^T X (T, N).
- * Requirements: m, n, k >= 0; lda >= max(1, transA == N ? k : m);
- * ldb >= max(1, transB == N ? n : k); ldc >= max(1, n); A, B non-NULL when
- * m*k resp. k*n > 0; C non-NULL when m*n > 0.  m == 0 or n == 0 launches
- * nothing; k == 0 writes +0.0f to C.
+ * Requirements: 0 <= m, n, k < 2^31; lda >= max(1, transA == N ? k : m);
+ * ldb >= max(1, transB == N ? n : k); ldc >= max(1, n); lda, ldb < 2^22
+ * (else PAM_ERROR_NOT_SUPPORTED); A, B non-NULL when m*k resp. k*n > 0;
+ * C non-NULL when m*n > 0.  m == 0 or n == 0 launches nothing; k == 0
+ * writes +0.0f to C.
  */
 pam_status_t pam_gemm(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
                       const float *A, int64_t lda, const float *B, int64_t ldb,
@@ -101,13 +102,16 @@ pam_status_t pam_gemm_batched(pam_op_t transA, pam_op_t transB, int64_t m, int64
                               int64_t batch, hipStream_t stream);
 
 /*
- * How a product is tiled: output tile tile_m x tile_n per workgroup, and the
- * number of K slices whose partial sums are added afterwards (1 = none).
+ * How a product is tiled: output tile tile_m x tile_n per workgroup;
+ * kgroups waves per micro-tile position that share each LDS chunk's k steps
+ * and add their partial tiles in LDS; and the number of K slices whose
+ * partial sums are added by a second kernel (1 = none).
  */
 typedef struct {
     int32_t tile_m;
     int32_t tile_n;
     int32_t splits;
+    int32_t kgroups;
 } pam_plan_t;
 
 /* The plan pam_gemm / pam_gemm_batched would use for these sizes. */
@@ -115,8 +119,9 @@ pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_p
 
 /*
  * pam_gemm_batched with an explicit plan (for tests and tuning).
- * tile_m, tile_n in {64, 128}; splits >= 1.  The result is the same
- * product as with the automatic plan, up to float32 summation order.
+ * (tile_m, tile_n, kgroups) is (128,128,1), (128,64,1), (64,64,1) or
+ * (64,64,4); 1 <= splits <= 64.  The result is the same product as with
+ * the automatic plan, up to float32 summation order.
  */
 pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB,
                                         int64_t m, int64_t n, int64_t k,

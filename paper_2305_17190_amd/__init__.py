@@ -35,7 +35,8 @@ class PamError(RuntimeError):
 
 
 class _Plan(ctypes.Structure):
-    _fields_ = [("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("splits", ctypes.c_int32)]
+    _fields_ = [("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("splits", ctypes.c_int32),
+                ("kgroups", ctypes.c_int32)]
 
 
 class _DeviceInfo(ctypes.Structure):
@@ -163,7 +164,8 @@ def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None):
 def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None):
     """Batched C[z] = op(A[z]) .^ op(B[z]) over the leading axis.
 
-    ``plan`` = (tile_m, tile_n, splits) forces a tiling (tests and tuning).
+    ``plan`` = (tile_m, tile_n, splits[, kgroups]) forces a tiling (tests
+    and tuning).
     """
     torch = _torch()
     _require(A, "A", 3)
@@ -186,16 +188,16 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None)
     if plan is None:
         _check(lib.pam_gemm_batched(*args, _stream_handle(A)))
     else:
-        p = _Plan(*plan)
+        p = _Plan(*plan) if len(plan) == 4 else _Plan(plan[0], plan[1], plan[2], 1)
         _check(lib.pam_gemm_batched_with_plan(*args, ctypes.byref(p), _stream_handle(A)))
     return out
 
 
 def plan(m: int, n: int, k: int, batch: int = 1):
-    """(tile_m, tile_n, splits) the library picks for these sizes."""
+    """(tile_m, tile_n, splits, kgroups) the library picks for these sizes."""
     p = _Plan()
     _check(load().pam_gemm_plan(m, n, k, batch, ctypes.byref(p)))
-    return (p.tile_m, p.tile_n, p.splits)
+    return (p.tile_m, p.tile_n, p.splits, p.kgroups)
 
 
 def device_info(device: int = 0) -> dict:

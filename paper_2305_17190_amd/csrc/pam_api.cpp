@@ -32,43 +32,77 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 constexpr int64_t kMaxDim = 0x7FFFFFFF;
 constexpr int64_t kMaxGridZ = 65535;
 constexpr int64_t kMaxSplits = 64;
-// Enough waves for about two per SIMD on a 256-CU device.
-constexpr int64_t kTargetWaves = 2048;
+// 128 rows of a panel, in bytes, must fit the kernels' 32-bit offsets.
+constexpr int64_t kMaxLd = (int64_t)1 << 22;
 
 struct Plan {
-    int tile_m, tile_n, splits;
+    int tile_m, tile_n, kgroups, splits;
     int64_t k_per_split;
 };
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Largest tile whose padding waste is small, then split K until the launch
-// has enough waves (each split keeps at least four LDS chunks).
-Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch) {
-    static const int cand[3][2] = {{128, 128}, {128, 64}, {64, 64}};
-    int bm = 64, bn = 64;
-    for (const auto &c : cand) {
-        const double waste = double(ceil_div(m, c[0]) * c[0]) * double(ceil_div(n, c[1]) * c[1]) / double(m * n);
-        if (waste <= 1.15) {
-            bm = c[0];
-            bn = c[1];
-            break;
-        }
-    }
-    const int64_t waves = ceil_div(m, bm) * ceil_div(n, bn) * batch * (bm * bn / 4096);
-    int64_t splits = 1;
-    if (waves > 0 && waves < kTargetWaves) {
-        const int64_t want = ceil_div(2 * kTargetWaves, waves);
-        const int64_t most = std::max<int64_t>(1, k / (4 * pamk::kChunkK));
-        splits = std::min(std::min(want, most), kMaxSplits);
-    }
-    Plan p{bm, bn, 1, k};
+struct Shape {
+    int bm, bn, kw;
+    double rate;    // sustained PAM-MACs per second with the device full (measured on MI355X)
+    int per_cu;     // workgroups resident per compute unit (registers and LDS)
+};
+// 128 x 128 and 128 x 64 tiles with one k-group; 64 x 64 tiles with one
+// k-group, or whose four waves split each chunk's k steps (four times the
+// waves without partial sums in HBM, at twice the staging work per MAC).
+const Shape kShapes[] = {{128, 128, 1, 21.5e12, 2},
+                         {128, 64, 1, 20.0e12, 4},
+                         {64, 64, 1, 20.0e12, 8},
+                         {64, 64, 4, 16.5e12, 2}};
+constexpr int kComputeUnits = 256;
+constexpr double kWorkgroupFixedS = 8e-6;   // first loads, epilogue stores
+constexpr double kSplitFixedS = 6e-6;       // second launch
+constexpr double kPartialBytesPerS = 3e12;  // writing and re-reading partial sums
+
+Plan make_plan(const Shape &c, int64_t k, int64_t splits) {
+    Plan p{c.bm, c.bn, c.kw, 1, k};
     if (splits > 1) {
-        const int64_t per = ceil_div(ceil_div(k, splits), pamk::kChunkK) * pamk::kChunkK;
+        const int64_t per = ceil_div(ceil_div(k, splits), pamk::kChunkK * c.kw) * pamk::kChunkK * c.kw;
         p.k_per_split = per;
         p.splits = (int)ceil_div(k, per);
     }
     return p;
+}
+
+// Estimated time: rounds of resident workgroups, each a fixed cost plus its
+// chunks at the shape's rate, plus for split-K a second launch and the
+// partial sums' round trip through memory.
+double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t batch) {
+    const int64_t bk = pamk::kChunkK * c.kw;
+    const int64_t chunks = ceil_div(p.k_per_split, bk);
+    const int64_t wgs = ceil_div(m, c.bm) * ceil_div(n, c.bn) * batch * p.splits;
+    const int64_t rounds = ceil_div(wgs, (int64_t)c.per_cu * kComputeUnits);
+    const double chunk_s = double(c.bm) * c.bn * bk * c.per_cu * kComputeUnits / c.rate;
+    double t = double(rounds) * (kWorkgroupFixedS + double(chunks) * chunk_s);
+    if (p.splits > 1)
+        t += kSplitFixedS + double(p.splits + 1) * double(m) * double(n) * double(batch) * 4.0 / kPartialBytesPerS;
+    return t;
+}
+
+// The cheapest (shape, split) by plan_time; splits keep at least four
+// chunks each.
+Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch) {
+    double best_t = 0.0;
+    Plan best{};
+    bool have = false;
+    for (const auto &c : kShapes) {
+        const int64_t most = std::max<int64_t>(1, std::min(kMaxSplits, k / (4 * pamk::kChunkK * c.kw)));
+        for (int64_t s = 1; s <= most; s *= 2) {
+            const Plan p = make_plan(c, k, s);
+            const double t = plan_time(c, p, m, n, batch);
+            if (!have || t < best_t) {
+                best_t = t;
+                best = p;
+                have = true;
+            }
+        }
+    }
+    return best;
 }
 
 pam_status_t validate(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
@@ -86,6 +120,8 @@ pam_status_t validate(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
         return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
     if (sa < 0 || sb < 0 || sc < 0)
         return fail(PAM_ERROR_INVALID_VALUE, "batch strides must be >= 0");
+    if (lda > kMaxLd || ldb > kMaxLd)
+        return fail(PAM_ERROR_NOT_SUPPORTED, "lda and ldb must be below 2^22 (per-thread 32-bit offsets)");
     const int64_t min_lda = std::max<int64_t>(1, ta == PAM_OP_N ? k : m);
     const int64_t min_ldb = std::max<int64_t>(1, tb == PAM_OP_N ? n : k);
     const int64_t min_ldc = std::max<int64_t>(1, n);
@@ -184,7 +220,8 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
         p.C = C + b0 * sc;
         p.W = ws;
         p.vec_c = ws ? (n % 4 == 0) : (aligned16(C) && ldc % 4 == 0 && (batch == 1 || sc % 4 == 0));
-        hipError_t e = pamk::launch_pam_gemm(plan.tile_m, plan.tile_n, ta == PAM_OP_T, tb == PAM_OP_T, p, nb, stream);
+        hipError_t e = pamk::launch_pam_gemm(plan.tile_m, plan.tile_n, plan.kgroups, ta == PAM_OP_T, tb == PAM_OP_T, p,
+                                             nb, stream);
         if (e != hipSuccess) {
             result = fail_hip(e, "gemm kernel launch");
             break;
@@ -283,6 +320,7 @@ pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_p
     plan->tile_m = p.tile_m;
     plan->tile_n = p.tile_n;
     plan->splits = p.splits;
+    plan->kgroups = p.kgroups;
     return PAM_SUCCESS;
 }
 
@@ -295,15 +333,18 @@ pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB, int64_
         return st;
     if (plan == nullptr)
         return fail(PAM_ERROR_INVALID_VALUE, "plan is NULL");
-    const bool tile_ok = (plan->tile_m == 128 && plan->tile_n == 128) || (plan->tile_m == 128 && plan->tile_n == 64) ||
-                         (plan->tile_m == 64 && plan->tile_n == 64);
+    const bool tile_ok = (plan->kgroups == 1 && ((plan->tile_m == 128 && plan->tile_n == 128) ||
+                                                 (plan->tile_m == 128 && plan->tile_n == 64) ||
+                                                 (plan->tile_m == 64 && plan->tile_n == 64))) ||
+                         (plan->kgroups == 4 && plan->tile_m == 64 && plan->tile_n == 64);
     if (!tile_ok)
-        return fail(PAM_ERROR_INVALID_VALUE, "tile must be 128x128, 128x64 or 64x64");
+        return fail(PAM_ERROR_INVALID_VALUE,
+                    "(tile_m, tile_n, kgroups) must be (128,128,1), (128,64,1), (64,64,1) or (64,64,4)");
     if (plan->splits < 1 || plan->splits > kMaxSplits)
         return fail(PAM_ERROR_INVALID_VALUE, "splits must be in [1, 64]");
     if (m == 0 || n == 0 || batch == 0)
         return PAM_SUCCESS;
-    Plan p{plan->tile_m, plan->tile_n, 1, std::max<int64_t>(k, 1)};
+    Plan p{plan->tile_m, plan->tile_n, plan->kgroups, 1, std::max<int64_t>(k, 1)};
     if (plan->splits > 1 && k > 0) {
         const int64_t per = ceil_div(ceil_div(k, plan->splits), pamk::kChunkK) * pamk::kChunkK;
         p.k_per_split = per;

@@ -29,8 +29,9 @@ struct GemmParams {
 
 hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
 
-// tile_m, tile_n in {64, 128}; grid = (tiles_m * tiles_n, splits, batch_in_launch).
-hipError_t launch_pam_gemm(int tile_m, int tile_n, bool trans_a, bool trans_b,
+// (tile_m, tile_n, kgroups) in {(128,128,1), (128,64,1), (64,64,1), (64,64,4)};
+// grid = (tiles_m * tiles_n, splits, batch_in_launch).
+hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b,
                            const GemmParams &p, int64_t batch, hipStream_t stream);
 
 // C[b][i][j] = sum_s W[b][s][i][j], s in increasing order.

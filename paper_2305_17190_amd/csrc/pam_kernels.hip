@@ -147,132 +147,162 @@ hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n,
 // Tiled PAM matrix product
 // ---------------------------------------------------------------------------
 
-// An operand tile of D (rows of op(A), or columns of op(B)) x kChunkK staged
-// through registers.  KCONTIG: element (o, kk) of the tile sits at
-// base[(o0 + o) * ld + k0 + kk] (A with op N, B with op T); otherwise at
-// base[(k0 + kk) * ld + o0 + o] (A with op T, B with op N).  Each thread
-// holds L float4 groups of four consecutive elements of the contiguous axis.
-template <int D, int NT, bool KCONTIG>
+// An operand tile of D (rows of op(A), or columns of op(B)) x kChunkK, staged
+// through registers.  KCONTIG: element (o, kk) of chunk c sits at
+// base + (o0 + o) * ld + k0 + kk (A with op N, B with op T); otherwise at
+// base + (k0 + kk) * ld + o0 + o (A with op T, B with op N).  Each thread
+// holds L groups of four elements consecutive in memory.  The byte offset of
+// each group from the chunk's base is fixed for the whole K loop, so the base
+// (uniform, in scalar registers) is the only address that moves.
+template <int D, int NT, int BK, bool KCONTIG>
 struct TileLoader {
-    static constexpr int BK = kChunkK;
     static constexpr int L = D * BK / 4 / NT;
     static_assert(L >= 1 && D * BK / 4 == L * NT, "tile does not divide over the threads");
     uint4 v[L];
+    uint32_t boff[L];   // byte offset of the group from the chunk base
+    uint32_t edge;      // bit r: group r straddles the last valid row (OCONTIG) -- per-element path
+
+    // Group r of thread tid: KCONTIG -> (row o, k offset kq); else (k row kk, first o oq).
+    static __device__ __forceinline__ int grp_o(int tid, int r) {
+        const int f = tid + NT * r;
+        return KCONTIG ? f / (BK / 4) : (f % (D / 4)) * 4;
+    }
+    static __device__ __forceinline__ int grp_k(int tid, int r) {
+        const int f = tid + NT * r;
+        return KCONTIG ? (f % (BK / 4)) * 4 : f / (D / 4);
+    }
 
     // Rows past o_lim are clamped to the last valid row (their outputs are
-    // discarded); elements at k >= k_lim are zero (they must add nothing).
-    __device__ __forceinline__ void load(const float *__restrict__ base, int64_t ld, int o0, int o_lim,
-                                         int k0, int k_lim, bool vec, int tid) {
+    // discarded); the clamp is fixed for the whole K loop.
+    __device__ __forceinline__ void init(int64_t ld, int o0, int o_lim, int tid) {
+        edge = 0;
 #pragma unroll
         for (int r = 0; r < L; ++r) {
-            const int f = tid + NT * r;
-            uint32_t e[4];
+            const int o = grp_o(tid, r);
+            const int kk = grp_k(tid, r);
             if (KCONTIG) {
-                const int o = min(o0 + f / (BK / 4), o_lim - 1);
-                const int kq = k0 + (f % (BK / 4)) * 4;
-                const float *src = base + (int64_t)o * ld + kq;
-                if (vec && kq + 3 < k_lim) {
-                    const uint4 q = *reinterpret_cast<const uint4 *>(src);
-                    e[0] = q.x; e[1] = q.y; e[2] = q.z; e[3] = q.w;
-                } else {
-#pragma unroll
-                    for (int c = 0; c < 4; ++c)
-                        e[c] = (kq + c < k_lim) ? __float_as_uint(src[c]) : 0u;
-                }
+                const int row = min(o0 + o, o_lim - 1) - o0;
+                boff[r] = (uint32_t)((row * ld + kk) * 4);
             } else {
-                const int kk = k0 + f / (D / 4);
-                const int oq = o0 + (f % (D / 4)) * 4;
-                if (kk < k_lim) {
-                    const float *row = base + (int64_t)kk * ld;
-                    if (vec && oq + 3 < o_lim) {
-                        const uint4 q = *reinterpret_cast<const uint4 *>(row + oq);
-                        e[0] = q.x; e[1] = q.y; e[2] = q.z; e[3] = q.w;
-                    } else {
-#pragma unroll
-                        for (int c = 0; c < 4; ++c)
-                            e[c] = __float_as_uint(row[min(oq + c, o_lim - 1)]);
-                    }
-                } else {
-                    e[0] = e[1] = e[2] = e[3] = 0u;
-                }
+                boff[r] = (uint32_t)((kk * ld + o) * 4);
+                if (o0 + o + 3 >= o_lim)
+                    edge |= 1u << r;
             }
-            v[r] = make_uint4(e[0], e[1], e[2], e[3]);
         }
     }
 
-    // Nonzero when some element needs the SPECIAL path: inf, NaN or |x| >= 2^64.
-    __device__ __forceinline__ uint32_t needs_special() const {
-        uint32_t any = 0;
+    // Load chunk elements [k0, k0 + BK) of the panel whose chunk base is
+    // `base`.  Elements at k >= k_lim are zero (they must add nothing).
+    __device__ __forceinline__ void load(const float *__restrict__ base, int o0, int o_lim, int k0, int k_lim,
+                                         bool vec, int tid) {
+        const char *cb = reinterpret_cast<const char *>(base);
+        if (vec && k0 + BK <= k_lim) {
+            // Interior chunk, aligned operand: one 16-byte load per group.
+#pragma unroll
+            for (int r = 0; r < L; ++r) {
+                if (KCONTIG || !((edge >> r) & 1u))
+                    v[r] = *reinterpret_cast<const uint4 *>(cb + boff[r]);
+                else
+                    v[r] = load_elements(cb, r, o0, o_lim, k0, k_lim, tid);
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < L; ++r)
+                v[r] = load_elements(cb, r, o0, o_lim, k0, k_lim, tid);
+        }
+    }
+
+    // Group r element by element, with the K tail and (OCONTIG) the last
+    // valid row applied.
+    __device__ __forceinline__ uint4 load_elements(const char *cb, int r, int o0, int o_lim, int k0, int k_lim,
+                                                   int tid) const {
+        const float *src = reinterpret_cast<const float *>(cb + boff[r]);
+        const int kk = grp_k(tid, r);
+        uint32_t e[4];
+        if (KCONTIG) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                e[c] = (k0 + kk + c < k_lim) ? __float_as_uint(src[c]) : 0u;
+        } else {
+            const int o = grp_o(tid, r);
+            const float *row = src - o;
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                e[c] = (k0 + kk < k_lim) ? __float_as_uint(row[min(o0 + o + c, o_lim - 1) - o0]) : 0u;
+        }
+        return make_uint4(e[0], e[1], e[2], e[3]);
+    }
+
+    // Scan the held elements.  Returns bit 0 when some element is "tiny" (a
+    // normal number with exponent field 1..63, whose products can
+    // underflow) and bit 1 when some element needs the SPECIAL path (inf, NaN
+    // or |x| >= 2^64).  Zeros and denormals are neither.
+    __device__ __forceinline__ uint32_t scan() const {
+        uint32_t hi = 0, lo = 0xFFFFFFFFu;
 #pragma unroll
         for (int r = 0; r < L; ++r) {
             const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-                any |= (e[c] & kMag) >= 0x5F800000u;
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t ex = e[c] & kExpMask;
+                hi = max(hi, ex);
+                lo = min(lo, ex - kMinNormal);   // a zero field wraps to the top
+            }
         }
-        return any;
+        return (lo < (63u << 23) ? 1u : 0u) | (hi >= (191u << 23) ? 2u : 0u);
     }
 
-    // "Tiny": a normal number with exponent field 1..63, whose products can
-    // underflow.  Zeros and denormals are not tiny (their products are exact
-    // zeros in both S2 and S3).
+    // "Tiny": a normal number with exponent field 1..63.
     __device__ __forceinline__ static bool tiny(uint32_t u) {
         return (u & kExpMask) - kMinNormal < (63u << 23);
     }
 
-    // Write the chunk into LDS, k-major: s[plane][kk][o].  SCALED: A gets
-    // plane 0 = aM, plane 1 = m; B gets plane 0 = b'.  SPECIAL: raw words in
-    // plane 0.  Tiny elements set bit kk of mask[w] (A: the wave that reads
-    // row o, from row_wave; B: mask[b_slot], read by every wave).
+    // Write the chunk into LDS buffer s, k-major: s[plane][kk][o].  A: plane 0
+    // aM (1 + M), plane 1 m (+-2^E or +-0); B: plane 0 b' (b - bias, zero and
+    // denormal b as a signed zero first).  When `has_tiny`, a tiny element at
+    // chunk step k sets bit k % 16 of mask[(k / 16) * (b_slot + 1) + w], w
+    // being the row wave that reads it (A) or b_slot (B).
     template <int LDS_LD, typename RowWave>
-    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], int mode, bool is_b, int tid, uint32_t *mask,
-                                          int b_slot, RowWave row_wave) const {
+    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], bool is_b, int tid, bool has_tiny,
+                                          uint32_t *mask, int b_slot, RowWave row_wave) const {
 #pragma unroll
         for (int r = 0; r < L; ++r) {
-            const int f = tid + NT * r;
             const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
             uint32_t p0[4], p1[4];
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const uint32_t u = e[c];
-                if (mode == kSpecial) {
-                    p0[c] = u;
-                    p1[c] = 0u;
-                } else if (is_b) {
-                    const uint32_t z = ((u & kExpMask) == 0u) ? (u & kSign) : u;   // denormal -> signed zero
-                    p0[c] = z - kBias;
+                if (is_b) {
+                    p0[c] = (((u & kExpMask) == 0u) ? (u & kSign) : u) - kBias;
                     p1[c] = 0u;
                 } else {
                     p0[c] = (u & kMant) | kBias;
                     p1[c] = u & kSignExp;
                 }
             }
-            int o, kk0;
+            const int o = grp_o(tid, r);
+            const int kk = grp_k(tid, r);
             if (KCONTIG) {
-                o = f / (BK / 4);
-                kk0 = (f % (BK / 4)) * 4;
 #pragma unroll
                 for (int c = 0; c < 4; ++c)
-                    s[0][kk0 + c][o] = p0[c];
-                if (!is_b && mode != kSpecial) {
+                    s[0][kk + c][o] = p0[c];
+                if (!is_b) {
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
-                        s[1][kk0 + c][o] = p1[c];
+                        s[1][kk + c][o] = p1[c];
                 }
             } else {
-                kk0 = f / (D / 4);
-                o = (f % (D / 4)) * 4;
-                *reinterpret_cast<uint4 *>(&s[0][kk0][o]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
-                if (!is_b && mode != kSpecial)
-                    *reinterpret_cast<uint4 *>(&s[1][kk0][o]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
+                *reinterpret_cast<uint4 *>(&s[0][kk][o]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
+                if (!is_b)
+                    *reinterpret_cast<uint4 *>(&s[1][kk][o]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
             }
-            if (mode != kSpecial) {
+            if (has_tiny) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     if (tiny(e[c])) {
-                        const int kk = KCONTIG ? kk0 + c : kk0;
-                        const int oc = KCONTIG ? o : o + c;
-                        atomicOr(&mask[is_b ? b_slot : row_wave(oc)], 1u << kk);
+                        const int k = KCONTIG ? kk + c : kk;
+                        atomicOr(&mask[(k / 16) * (b_slot + 1) + (is_b ? b_slot : row_wave(KCONTIG ? o : o + c))],
+                                 1u << (k % 16));
                     }
                 }
             }
@@ -280,22 +310,73 @@ struct TileLoader {
     }
 };
 
-// S3 update of a micro-tile: the product t * m is rounded (denormal results
-// flushed) before it is added, never fused into an fma.
-__device__ __forceinline__ void s3_accumulate(float (&acc)[8][8], const uint32_t (&am)[8], const uint32_t (&mm)[8],
-                                              const uint32_t (&bb)[8]) {
-#pragma clang fp contract(off)
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const float prod = __uint_as_float(am[i] + bb[j]) * __uint_as_float(mm[i]);
-            acc[i][j] = acc[i][j] + prod;
-        }
+// One micro-tile row, S2: acc[j] = fma(aM + b'[j], m, acc[j]) for j < 8.
+// The eight integer adds are issued before the eight fmas: a SIMD pairs the
+// full-rate ops of two waves only when neither wave stalls on the result of
+// its previous instruction, which a strict add/fma alternation would do.
+__device__ __forceinline__ void s2_row(float (&acc)[8], uint32_t am, uint32_t m, const uint32_t (&bb)[8]) {
+    uint32_t t0, t1, t2, t3, t4, t5, t6, t7;
+    asm("v_add_u32 %0, %16, %18\n\t"
+        "v_add_u32 %1, %16, %19\n\t"
+        "v_add_u32 %2, %16, %20\n\t"
+        "v_add_u32 %3, %16, %21\n\t"
+        "v_add_u32 %4, %16, %22\n\t"
+        "v_add_u32 %5, %16, %23\n\t"
+        "v_add_u32 %6, %16, %24\n\t"
+        "v_add_u32 %7, %16, %25\n\t"
+        "v_fmac_f32 %8, %0, %17\n\t"
+        "v_fmac_f32 %9, %1, %17\n\t"
+        "v_fmac_f32 %10, %2, %17\n\t"
+        "v_fmac_f32 %11, %3, %17\n\t"
+        "v_fmac_f32 %12, %4, %17\n\t"
+        "v_fmac_f32 %13, %5, %17\n\t"
+        "v_fmac_f32 %14, %6, %17\n\t"
+        "v_fmac_f32 %15, %7, %17"
+        : "=&v"(t0), "=&v"(t1), "=&v"(t2), "=&v"(t3), "=&v"(t4), "=&v"(t5), "=&v"(t6), "=&v"(t7),
+          "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(acc[4]), "+v"(acc[5]), "+v"(acc[6]),
+          "+v"(acc[7])
+        : "v"(am), "v"(m), "v"(bb[0]), "v"(bb[1]), "v"(bb[2]), "v"(bb[3]), "v"(bb[4]), "v"(bb[5]), "v"(bb[6]),
+          "v"(bb[7]));
 }
 
-template <int LD>
-__device__ __forceinline__ void lds_frag(const uint32_t (*s)[kChunkK][LD], int plane, int kk, int i0, int half,
+// One micro-tile row, S3: p = (aM + b'[j]) * m rounded on its own (an
+// underflowing product is flushed to zero), then acc[j] += p; each of the
+// three ops is issued for all eight columns before the next.
+__device__ __forceinline__ void s3_row(float (&acc)[8], uint32_t am, uint32_t m, const uint32_t (&bb)[8]) {
+    uint32_t t0, t1, t2, t3, t4, t5, t6, t7;
+    asm("v_add_u32 %0, %16, %18\n\t"
+        "v_add_u32 %1, %16, %19\n\t"
+        "v_add_u32 %2, %16, %20\n\t"
+        "v_add_u32 %3, %16, %21\n\t"
+        "v_add_u32 %4, %16, %22\n\t"
+        "v_add_u32 %5, %16, %23\n\t"
+        "v_add_u32 %6, %16, %24\n\t"
+        "v_add_u32 %7, %16, %25\n\t"
+        "v_mul_f32 %0, %0, %17\n\t"
+        "v_mul_f32 %1, %1, %17\n\t"
+        "v_mul_f32 %2, %2, %17\n\t"
+        "v_mul_f32 %3, %3, %17\n\t"
+        "v_mul_f32 %4, %4, %17\n\t"
+        "v_mul_f32 %5, %5, %17\n\t"
+        "v_mul_f32 %6, %6, %17\n\t"
+        "v_mul_f32 %7, %7, %17\n\t"
+        "v_add_f32 %8, %8, %0\n\t"
+        "v_add_f32 %9, %9, %1\n\t"
+        "v_add_f32 %10, %10, %2\n\t"
+        "v_add_f32 %11, %11, %3\n\t"
+        "v_add_f32 %12, %12, %4\n\t"
+        "v_add_f32 %13, %13, %5\n\t"
+        "v_add_f32 %14, %14, %6\n\t"
+        "v_add_f32 %15, %15, %7"
+        : "=&v"(t0), "=&v"(t1), "=&v"(t2), "=&v"(t3), "=&v"(t4), "=&v"(t5), "=&v"(t6), "=&v"(t7),
+          "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(acc[4]), "+v"(acc[5]), "+v"(acc[6]),
+          "+v"(acc[7])
+        : "v"(am), "v"(m), "v"(bb[0]), "v"(bb[1]), "v"(bb[2]), "v"(bb[3]), "v"(bb[4]), "v"(bb[5]), "v"(bb[6]),
+          "v"(bb[7]));
+}
+
+template <int BK, int LD>
+__device__ __forceinline__ void lds_frag(const uint32_t (*s)[BK][LD], int plane, int kk, int i0, int half,
                                          uint32_t out[8]) {
     const uint4 lo = *reinterpret_cast<const uint4 *>(&s[plane][kk][i0]);
     const uint4 hi = *reinterpret_cast<const uint4 *>(&s[plane][kk][half + i0]);
@@ -303,41 +384,68 @@ __device__ __forceinline__ void lds_frag(const uint32_t (*s)[kChunkK][LD], int p
     out[4] = hi.x; out[5] = hi.y; out[6] = hi.z; out[7] = hi.w;
 }
 
-template <int BM, int BN, bool TA, bool TB>
-__global__ void __launch_bounds__(BM * BN / 64) pam_gemm_kernel(GemmParams p) {
-    constexpr int BK = kChunkK;
-    constexpr int NT = BM * BN / 64;
+// One workgroup computes a BM x BN output tile.  Each of its KW k-groups
+// holds the whole tile in 8 x 8 register micro-tiles (BM * BN / 64 threads)
+// and takes 16 of the 16 * KW k steps of every LDS chunk; with KW > 1 the
+// groups' partial tiles are added through LDS at the end, so small outputs
+// get more waves without extra HBM traffic.
+template <int BM, int BN, int KW, bool TA, bool TB>
+__global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(2)))
+pam_gemm_kernel(GemmParams p) {
+    constexpr int KPG = kChunkK;           // k steps per group per chunk
+    constexpr int BK = KPG * KW;           // chunk depth
+    constexpr int NTG = BM * BN / 64;      // threads per k-group
+    constexpr int NT = NTG * KW;
     constexpr int NW = NT / 64;
+    constexpr int NRW = NTG / 64;          // waves per k-group
     constexpr int TXN = BN / 8;            // threads along n
     constexpr int TY_PER_WAVE = 64 / TXN;  // micro-tile rows (of 2 x 4) per wave
     constexpr int HM = BM / 2;
     constexpr int HN = BN / 2;
     constexpr int LDA = BM + 4;            // padded LDS rows, 16-byte aligned
     constexpr int LDB = BN + 4;
+    constexpr int LDR = BN + 4;            // partial-tile rows (KW > 1)
+    static_assert(NTG % 64 == 0, "bad tile shape");
 
-    __shared__ uint32_t sA[2][BK][LDA];    // SCALED: plane 0 aM, plane 1 m; SPECIAL: plane 0 raw
-    __shared__ uint32_t sB[1][BK][LDB];    // SCALED: b'; SPECIAL: raw
-    __shared__ uint32_t sVote[NW];
-    __shared__ uint32_t sMask[2][NW + 1];  // per chunk parity: tiny bits per wave (A rows) and for B
+    // The chunk in LDS, and for KW > 1 the partial tiles, which reuse the
+    // same bytes after the K loop.
+    constexpr int kTileWords = 2 * BK * LDA + BK * LDB;
+    constexpr int kRedWords = KW > 1 ? KW * BM * LDR : 0;
+    __shared__ __attribute__((aligned(16))) uint32_t smem[kTileWords > kRedWords ? kTileWords : kRedWords];
+    __shared__ uint32_t sVote[NW];                 // chunk needs the SPECIAL path
+    __shared__ uint32_t sMask[2][KW * (NRW + 1)];  // [chunk parity] tiny bits per (group, row wave / B)
+    uint32_t (*sA)[BK][LDA] = reinterpret_cast<uint32_t (*)[BK][LDA]>(smem);             // plane 0 aM, 1 m
+    uint32_t (*sB)[BK][LDB] = reinterpret_cast<uint32_t (*)[BK][LDB]>(smem + 2 * BK * LDA);  // b'
 
     const int tid = threadIdx.x;
-    const int tx = tid % TXN;
-    const int ty = tid / TXN;
+    const int grp = tid / NTG;
+    const int t = tid % NTG;
+    const int tx = t % TXN;
+    const int ty = t / TXN;
     const int wave = tid >> 6;
+    const int rwave = t >> 6;
     const int tm = blockIdx.x / p.tiles_n;
     const int tn = blockIdx.x % p.tiles_n;
     const int m0 = tm * BM;
     const int n0 = tn * BN;
     const int split = blockIdx.y;
     const int64_t bz = blockIdx.z;
-    const float *A = p.A + bz * p.strideA;
-    const float *B = p.B + bz * p.strideB;
     const int kb = split * p.k_per_split;
     const int ke = min(p.k, kb + p.k_per_split);
     const int nchunks = ke > kb ? (ke - kb + BK - 1) / BK : 0;
 
-    TileLoader<BM, NT, !TA> la;
-    TileLoader<BN, NT, TB> lb;
+    // Chunk bases (uniform): op(A) rows m0.., op(B) columns n0.., at k = kb.
+    const float *a_base = p.A + bz * p.strideA + (TA ? (int64_t)kb * p.lda + m0 : (int64_t)m0 * p.lda + kb);
+    const float *b_base = p.B + bz * p.strideB + (TB ? (int64_t)n0 * p.ldb + kb : (int64_t)kb * p.ldb + n0);
+    const int64_t a_step = TA ? (int64_t)BK * p.lda : BK;
+    const int64_t b_step = TB ? BK : (int64_t)BK * p.ldb;
+    const bool vec_a = p.vec_a != 0;
+    const bool vec_b = p.vec_b != 0;
+
+    TileLoader<BM, NT, BK, !TA> la;
+    TileLoader<BN, NT, BK, TB> lb;
+    la.init(p.lda, m0, p.m, tid);
+    lb.init(p.ldb, n0, p.n, tid);
     auto row_wave = [](int o) { return ((o % HM) / 4) / TY_PER_WAVE; };
 
     float acc[8][8];
@@ -347,82 +455,93 @@ __global__ void __launch_bounds__(BM * BN / 64) pam_gemm_kernel(GemmParams p) {
         for (int j = 0; j < 8; ++j)
             acc[i][j] = 0.0f;
 
-    if (tid < 2 * (NW + 1))
+    if (tid < 2 * KW * (NRW + 1))
         (&sMask[0][0])[tid] = 0u;
 
     if (nchunks > 0) {
-        la.load(A, p.lda, m0, p.m, kb, ke, p.vec_a != 0, tid);
-        lb.load(B, p.ldb, n0, p.n, kb, ke, p.vec_b != 0, tid);
+        la.load(a_base, m0, p.m, kb, ke, vec_a, tid);
+        lb.load(b_base, n0, p.n, kb, ke, vec_b, tid);
     }
 
+    const int k_first = grp * KPG;
     for (int c = 0; c < nchunks; ++c) {
-        // Workgroup vote: SPECIAL if any operand of the chunk is inf, NaN or >= 2^64.
-        const uint64_t sp = __ballot(la.needs_special() | lb.needs_special());
+        const uint32_t f = la.scan() | lb.scan();
+        const uint64_t sp = __ballot(f & 2u);
+        const uint64_t tn_any = __ballot(f & 1u);
+        uint32_t *mask = sMask[c & 1];
+        __syncthreads();   // every wave is done reading the previous chunk (and zeroing this mask)
+        la.template store<LDA>(sA, false, tid, tn_any != 0, mask, NRW, row_wave);
+        lb.template store<LDB>(sB, true, tid, tn_any != 0, mask, NRW, row_wave);
         if ((tid & 63) == 0)
             sVote[wave] = sp ? 1u : 0u;
         __syncthreads();
+
         uint32_t v = 0;
 #pragma unroll
         for (int w = 0; w < NW; ++w)
             v |= sVote[w];
-        const int mode = v ? kSpecial : kScaled;
-
-        uint32_t *mask = sMask[c & 1];
-        if (tid < NW + 1)
-            sMask[(c + 1) & 1][tid] = 0u;   // next chunk's masks; last read two chunks ago
-        la.template store<LDA>(sA, mode, false, tid, mask, NW, row_wave);
-        lb.template store<LDB>(sB, mode, true, tid, mask, NW, row_wave);
-        __syncthreads();
+        const bool special = v != 0u;
+        const uint32_t slow =
+            __builtin_amdgcn_readfirstlane(mask[grp * (NRW + 1) + rwave] | mask[grp * (NRW + 1) + NRW]) & 0xFFFFu;
+        if (tid < KW * (NRW + 1))
+            sMask[(c + 1) & 1][tid] = 0u;   // next chunk's masks; last read one chunk ago
 
         if (c + 1 < nchunks) {
             const int k0 = kb + (c + 1) * BK;
-            la.load(A, p.lda, m0, p.m, k0, ke, p.vec_a != 0, tid);
-            lb.load(B, p.ldb, n0, p.n, k0, ke, p.vec_b != 0, tid);
+            la.load(a_base + (c + 1) * a_step, m0, p.m, k0, ke, vec_a, tid);
+            lb.load(b_base + (c + 1) * b_step, n0, p.n, k0, ke, vec_b, tid);
         }
 
-        if (mode == kScaled) {
+        const uint32_t (*cA)[BK][LDA] = sA;
+        const uint32_t (*cB)[BK][LDB] = sB;
+        if (!special) {
             // Accumulation order is free, so a wave runs its S2 k steps first
             // and its S3 k steps after them; neither loop body branches.
-            const uint32_t slow = __builtin_amdgcn_readfirstlane(mask[wave] | mask[NW]) & 0xFFFFu;
             auto s2_step = [&](int kk) {
                 uint32_t am[8], mm[8], bb[8];
-                lds_frag<LDA>(sA, 0, kk, ty * 4, HM, am);
-                lds_frag<LDA>(sA, 1, kk, ty * 4, HM, mm);
-                lds_frag<LDB>(sB, 0, kk, tx * 4, HN, bb);
+                lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
+                lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
+                lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
 #pragma unroll
                 for (int i = 0; i < 8; ++i)
-#pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        acc[i][j] = __builtin_fmaf(__uint_as_float(am[i] + bb[j]), __uint_as_float(mm[i]), acc[i][j]);
+                    s2_row(acc[i], am[i], mm[i], bb);
             };
             if (slow == 0u) {
 #pragma unroll
-                for (int kk = 0; kk < BK; ++kk)
-                    s2_step(kk);
+                for (int j = 0; j < KPG; ++j)
+                    s2_step(k_first + j);
             } else {
                 for (uint32_t todo = ~slow & 0xFFFFu; todo != 0u; todo &= todo - 1u)
-                    s2_step(__builtin_ctz(todo));
+                    s2_step(k_first + __builtin_ctz(todo));
                 for (uint32_t todo = slow; todo != 0u; todo &= todo - 1u) {
-                    // S3: the product is rounded (and flushed) before the add.
-                    const int kk = __builtin_ctz(todo);
+                    const int kk = k_first + __builtin_ctz(todo);
                     uint32_t am[8], mm[8], bb[8];
-                    lds_frag<LDA>(sA, 0, kk, ty * 4, HM, am);
-                    lds_frag<LDA>(sA, 1, kk, ty * 4, HM, mm);
-                    lds_frag<LDB>(sB, 0, kk, tx * 4, HN, bb);
-                    s3_accumulate(acc, am, mm, bb);
+                    lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
+                    lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
+                    lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i)
+                        s3_row(acc[i], am[i], mm[i], bb);
                 }
             }
         } else {
+            // SPECIAL: rebuild each operand's encoding (A: sign and exponent
+            // from m, mantissa from aM; B: b' + bias, denormals already zero)
+            // and apply the complete definition per MAC.
 #pragma unroll 1
-            for (int kk = 0; kk < BK; ++kk) {
-                uint32_t a[8], b[8];
-                lds_frag<LDA>(sA, 0, kk, ty * 4, HM, a);
-                lds_frag<LDB>(sB, 0, kk, tx * 4, HN, b);
+            for (int j = 0; j < KPG; ++j) {
+                const int kk = k_first + j;
+                uint32_t am[8], mm[8], bb[8];
+                lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
+                lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
+                lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
+                for (int i = 0; i < 8; ++i) {
+                    const uint32_t a = mm[i] | (am[i] & kMant);
 #pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        acc[i][j] += __uint_as_float(pam_full(a[i], b[j]));
+                    for (int j2 = 0; j2 < 8; ++j2)
+                        acc[i][j2] += __uint_as_float(pam_full(a, bb[j2] + kBias));
+                }
             }
         }
     }
@@ -437,52 +556,106 @@ __global__ void __launch_bounds__(BM * BN / 64) pam_gemm_kernel(GemmParams p) {
         out = p.C + bz * p.strideC;
         ld = p.ldc;
     }
+    if (KW == 1) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int row = m0 + (i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4));
-        if (row >= p.m)
-            continue;
-        float *orow = out + (int64_t)row * ld;
+        for (int i = 0; i < 8; ++i) {
+            const int row = m0 + (i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4));
+            if (row >= p.m)
+                continue;
+            float *orow = out + (int64_t)row * ld;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int col = n0 + (h == 0 ? tx * 4 : HN + tx * 4);
-            if (p.vec_c && col + 3 < p.n) {
-                *reinterpret_cast<float4 *>(orow + col) =
+            for (int h = 0; h < 2; ++h) {
+                const int col = n0 + (h == 0 ? tx * 4 : HN + tx * 4);
+                if (p.vec_c && col + 3 < p.n) {
+                    *reinterpret_cast<float4 *>(orow + col) =
+                        make_float4(acc[i][4 * h], acc[i][4 * h + 1], acc[i][4 * h + 2], acc[i][4 * h + 3]);
+                } else {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (col + j < p.n)
+                            orow[col + j] = acc[i][4 * h + j];
+                }
+            }
+        }
+    } else {
+        // Every group writes its partial tile over the chunk buffer (after a
+        // barrier: other waves may still be reading the last chunk); each
+        // thread then adds the KW partials, in group order, for BM * BN / NT
+        // outputs.
+        __syncthreads();
+        float *red = reinterpret_cast<float *>(smem);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int col = h == 0 ? tx * 4 : HN + tx * 4;
+                *reinterpret_cast<float4 *>(&red[(grp * BM + row) * LDR + col]) =
                     make_float4(acc[i][4 * h], acc[i][4 * h + 1], acc[i][4 * h + 2], acc[i][4 * h + 3]);
-            } else {
+            }
+        }
+        __syncthreads();
+        constexpr int PER = BM * BN / NT;   // outputs per thread, a multiple of 4
+        static_assert(PER % 4 == 0 && BN % PER == 0, "bad reduction split");
+        const int e0 = tid * PER;
+        const int row = e0 / BN;
+        const int col0 = e0 % BN;
+        const int grow = m0 + row;
+        if (grow < p.m) {
+            float *orow = out + (int64_t)grow * ld;
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
-                    if (col + j < p.n)
-                        orow[col + j] = acc[i][4 * h + j];
+            for (int q = 0; q < PER / 4; ++q) {
+                const int col = col0 + 4 * q;
+                float4 sum = *reinterpret_cast<const float4 *>(&red[row * LDR + col]);
+#pragma unroll
+                for (int g = 1; g < KW; ++g) {
+                    const float4 x = *reinterpret_cast<const float4 *>(&red[(g * BM + row) * LDR + col]);
+                    sum.x += x.x;
+                    sum.y += x.y;
+                    sum.z += x.z;
+                    sum.w += x.w;
+                }
+                const int gcol = n0 + col;
+                if (p.vec_c && gcol + 3 < p.n) {
+                    *reinterpret_cast<float4 *>(orow + gcol) = sum;
+                } else {
+                    const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        if (gcol + j < p.n)
+                            orow[gcol + j] = sv[j];
+                }
             }
         }
     }
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int KW>
 static hipError_t launch_tile(bool ta, bool tb, const GemmParams &p, dim3 grid, hipStream_t stream) {
-    const dim3 block(BM * BN / 64);
+    const dim3 block(BM * BN / 64 * KW);
     if (!ta && !tb)
-        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, false, false>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, false, false>), grid, block, 0, stream, p);
     else if (!ta && tb)
-        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, false, true>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, false, true>), grid, block, 0, stream, p);
     else if (ta && !tb)
-        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, true, false>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, true, false>), grid, block, 0, stream, p);
     else
-        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, true, true>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, true, true>), grid, block, 0, stream, p);
     return hipGetLastError();
 }
 
-hipError_t launch_pam_gemm(int tile_m, int tile_n, bool trans_a, bool trans_b, const GemmParams &p,
+hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, const GemmParams &p,
                            int64_t batch, hipStream_t stream) {
     const int64_t tiles_m = (p.m + tile_m - 1) / tile_m;
     const dim3 grid((unsigned)(tiles_m * p.tiles_n), (unsigned)p.splits, (unsigned)batch);
-    if (tile_m == 128 && tile_n == 128)
-        return launch_tile<128, 128>(trans_a, trans_b, p, grid, stream);
-    if (tile_m == 128 && tile_n == 64)
-        return launch_tile<128, 64>(trans_a, trans_b, p, grid, stream);
-    if (tile_m == 64 && tile_n == 64)
-        return launch_tile<64, 64>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 128 && tile_n == 128 && kgroups == 1)
+        return launch_tile<128, 128, 1>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 128 && tile_n == 64 && kgroups == 1)
+        return launch_tile<128, 64, 1>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 64 && tile_n == 64 && kgroups == 1)
+        return launch_tile<64, 64, 1>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 64 && tile_n == 64 && kgroups == 4)
+        return launch_tile<64, 64, 4>(trans_a, trans_b, p, grid, stream);
     return hipErrorInvalidValue;
 }
 

@@ -75,22 +75,34 @@ def test_empty_products_launch_nothing(lib):
 
 
 def test_plan_selection_is_host_logic(lib):
-    # Large square products use the 128x128 tile without split-K.
-    assert pam.plan(16384, 4096, 4096) == (128, 128, 1)
-    # Small output, long K: split-K.
-    tm, tn, s = pam.plan(768, 192, 12608)
-    assert s > 1 and (tm, tn) in ((128, 64), (64, 64), (128, 128))
-    # Ragged n = 192 avoids a 128-wide tile (33% padding).
-    assert pam.plan(12608, 192, 768)[1] == 64
+    # Large products use the 128x128 tile without split-K.
+    assert pam.plan(16384, 4096, 4096) == (128, 128, 1, 1)
+    assert pam.plan(4096, 4096, 16384) == (128, 128, 1, 1)
+    assert pam.plan(8192, 2048, 512) == (128, 128, 1, 1)
+    # Narrow outputs with long K split K; short-K batched narrow outputs use
+    # the 64x64 tile whose four waves share each chunk's k steps.
+    assert pam.plan(8192, 512, 2048)[2] > 1
+    assert pam.plan(768, 192, 12608)[2] >= 16
+    assert pam.plan(256, 64, 256, 256) == (64, 64, 1, 4)
+    for m, n, k, b in ((1, 1, 1, 1), (5, 7, 3, 1), (300, 1, 17, 1), (16, 16, 100000, 1), (64, 64, 0, 3)):
+        tm, tn, s, kg = pam.plan(m, n, k, b)
+        assert (tm, tn, kg) in ((128, 128, 1), (128, 64, 1), (64, 64, 1), (64, 64, 4))
+        assert 1 <= s <= 64
     with pytest.raises(pam.PamError):
         pam.plan(0, 4, 4)
 
 
-def test_with_plan_rejects_bad_tiles(lib):
-    P = pam._Plan(96, 64, 1)
+@pytest.mark.parametrize("plan", [(96, 64, 1, 1), (128, 128, 0, 1), (128, 128, 1, 4), (64, 64, 1, 2),
+                                  (64, 64, 65, 1)])
+def test_with_plan_rejects_bad_tiles(lib, plan):
+    P = pam._Plan(*plan)
     assert lib.pam_gemm_batched_with_plan(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1, ctypes.byref(P), None) == 1
-    P = pam._Plan(128, 128, 0)
-    assert lib.pam_gemm_batched_with_plan(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1, ctypes.byref(P), None) == 1
+
+
+def test_leading_dimension_limit(lib):
+    big = 1 << 23
+    assert gemm_call(lib, lda=big) == 3
+    assert b"2^22" in lib.pam_last_error()
 
 
 def test_binding_refuses_cpu_tensors():

@@ -15,7 +15,8 @@ from oracle import pam_ref
 
 pytestmark = pytest.mark.gpu
 
-PLANS = [(128, 128, 1), (128, 64, 1), (64, 64, 1), (128, 128, 3), (128, 64, 7), (64, 64, 2)]
+PLANS = [(128, 128, 1), (128, 64, 1), (64, 64, 1), (64, 64, 1, 4), (128, 128, 3), (128, 64, 7), (64, 64, 2),
+         (64, 64, 3, 4)]
 TRANS = [(False, False), (False, True), (True, False), (True, True)]
 
 
@@ -82,6 +83,7 @@ def test_plans_and_layouts_normal(plan, ta, tb):
                                    ("zeros_tiny", "specials")], ids=lambda k: "-".join(k))
 def test_encodings(kinds, ta, tb):
     run_case(130, 200, 100, ta, tb, kinds[0], kinds[1], plan=(128, 64, 2), seed=21)
+    run_case(130, 200, 100, ta, tb, kinds[0], kinds[1], plan=(64, 64, 1, 4), seed=22)
 
 
 @pytest.mark.parametrize("pad", [(4, 4, 4), (1, 3, 5), (0, 0, 1)])
@@ -156,9 +158,10 @@ def test_deterministic():
     g = np.random.default_rng(73)
     a = to_dev(g.standard_normal((1, 200, 900)).astype(np.float32))
     b = to_dev(g.standard_normal((1, 900, 120)).astype(np.float32))
-    c1 = pam.bmm(a, b, plan=(64, 64, 6))
-    c2 = pam.bmm(a, b, plan=(64, 64, 6))
-    assert torch.equal(c1.view(torch.int32), c2.view(torch.int32))
+    for plan in ((64, 64, 6), (64, 64, 3, 4)):
+        c1 = pam.bmm(a, b, plan=plan)
+        c2 = pam.bmm(a, b, plan=plan)
+        assert torch.equal(c1.view(torch.int32), c2.view(torch.int32))
 
 
 def test_linear_layer_forms_with_torch_views():
@@ -195,7 +198,8 @@ def pow2_operands(shape, seed, decoy_frac):
 
 @pytest.mark.parametrize("decoys", [(0.0, 0.0), (0.01, 0.0), (0.0, 0.01), (0.02, 0.02), (0.3, 0.3)],
                          ids=["none", "A", "B", "both", "dense"])
-@pytest.mark.parametrize("plan", [(128, 128, 1), (128, 64, 2), (64, 64, 1)], ids=lambda p: "x".join(map(str, p)))
+@pytest.mark.parametrize("plan", [(128, 128, 1), (128, 64, 2), (64, 64, 1), (64, 64, 1, 4), (64, 64, 2, 4)],
+                         ids=lambda p: "x".join(map(str, p)))
 @pytest.mark.parametrize("ta,tb", [(False, True), (True, False)], ids=["NT", "TN"])
 def test_exact_sums_underflowing_products_add_nothing(decoys, plan, ta, tb):
     """Every non-underflowing term is +-2^-114..2^-110 and the K = 300 sums

@@ -106,6 +106,48 @@ def cpu_baseline(workload_id: int, host, forms, target_s: float) -> dict:
     }
 
 
+def bench_elementwise(args, torch, wl, pam, dev) -> int:
+    """pam_mul on N elements: 8 bytes read and 4 written per element."""
+    n = args.elementwise
+    a, b = wl.pam_mul_inputs(n, 1000 + 3)
+    da, db = torch.from_numpy(a).to(dev), torch.from_numpy(b).to(dev)
+    out = torch.empty_like(da)
+    for _ in range(args.warmup):
+        pam.mul(da, db, out=out)
+    torch.cuda.synchronize()
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    s.record()
+    for _ in range(args.steps):
+        pam.mul(da, db, out=out)
+    e.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    launch_s = s.elapsed_time(e) / 1e3 / args.steps
+    gbs = 12.0 * n / launch_s / 1e9
+    result = {
+        "metric": "elementwise pam_mul throughput",
+        "value": round(n / launch_s / 1e9, 3),
+        "unit": "G PAM/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": f"pam_mul n={n}, N(0,1) with 1% zeros and 1% powers of two"},
+        "roofline": {"bound": "hbm", "kernel": "pam_mul_vec4_kernel", "achieved": round(gbs, 1),
+                     "peak": 8000.0, "unit": "GB/s", "frac": round(gbs / 8000.0, 4), "traffic": None,
+                     "bytes_per_element": 12, "avg_launch_ms": round(launch_s * 1e3, 5)},
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -116,6 +158,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (reference kernel for HBM counters)")
+    ap.add_argument("--elementwise", type=int, default=0, metavar="N",
+                    help="time only elementwise pam_mul on N elements (HBM roofline) and print its line")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -142,6 +186,8 @@ def main() -> int:
         log(f"copied 3 x {src.numel() * 4} bytes")
         return 0
     pam.load()
+    if args.elementwise:
+        return bench_elementwise(args, torch, wl, pam, dev)
 
     wid = int(args.workload[1:])
     spec = wl.WORKLOADS[wid]

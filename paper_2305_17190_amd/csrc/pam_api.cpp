@@ -44,20 +44,42 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct Shape {
     int bm, bn, kw;
-    double rate;    // sustained PAM-MACs per second with the device full (measured on MI355X)
-    int per_cu;     // workgroups resident per compute unit (registers and LDS)
+    int waves;      // waves per workgroup
+    int per_cu;     // workgroups resident per compute unit (register budget)
+    double rate;    // PAM-MACs per second with every compute unit full (fitted to MI355X runs)
 };
 // 128 x 128 and 128 x 64 tiles with one k-group; 64 x 64 tiles with one
 // k-group, or whose four waves split each chunk's k steps (four times the
 // waves without partial sums in HBM, at twice the staging work per MAC).
-const Shape kShapes[] = {{128, 128, 1, 21.5e12, 2},
-                         {128, 64, 1, 20.0e12, 4},
-                         {64, 64, 1, 20.0e12, 8},
-                         {64, 64, 4, 16.5e12, 2}};
+// The 128 x 128 tile holds three waves per SIMD, the others two.
+const Shape kShapes[] = {{128, 128, 1, 4, 3, 24.3e12},
+                         {128, 64, 1, 2, 4, 19.5e12},
+                         {64, 64, 1, 1, 8, 18.1e12},
+                         {64, 64, 4, 4, 2, 17.2e12}};
 constexpr int kComputeUnits = 256;
-constexpr double kWorkgroupFixedS = 8e-6;   // first loads, epilogue stores
-constexpr double kSplitFixedS = 6e-6;       // second launch
-constexpr double kPartialBytesPerS = 3e12;  // writing and re-reading partial sums
+constexpr int kSimdsPerCu = 4;
+// Vector-ALU throughput of one SIMD holding 0..3 waves of this kernel,
+// relative to three: one wave issues alone, two pair their adds and fmas
+// but leave barrier and LDS waits exposed.
+constexpr double kSimdEfficiency[4] = {0.0, 0.421, 0.808, 1.0};
+constexpr double kWorkgroupFixedS = 3.4e-6;  // first loads, epilogue stores
+constexpr double kSplitFixedS = 9.6e-6;      // second launch
+constexpr double kPartialBytesPerS = 7.1e12; // writing and re-reading partial sums
+// Workgroups start as soon as slots free up, so a partial last round costs
+// less than a full one the more rounds precede it (they end staggered).
+constexpr double kTailDamping = 0.457;
+// Split-K plans must beat the best unsplit plan by this factor (they change
+// the summation order and take a workspace).
+constexpr double kSplitMargin = 0.97;
+// Split counts the plan search considers.
+constexpr int kSplitChoices[] = {1, 2, 3, 4, 5, 6, 7, 8, 12, 16, 24, 32, 48, 64};
+
+double cu_efficiency(int waves_per_cu) {
+    const int base = waves_per_cu / kSimdsPerCu;
+    const int extra = waves_per_cu % kSimdsPerCu;
+    return (extra * kSimdEfficiency[std::min(base + 1, 3)] + (kSimdsPerCu - extra) * kSimdEfficiency[std::min(base, 3)]) /
+           kSimdsPerCu;
+}
 
 Plan make_plan(const Shape &c, int64_t k, int64_t splits) {
     Plan p{c.bm, c.bn, c.kw, 1, k};
@@ -69,16 +91,26 @@ Plan make_plan(const Shape &c, int64_t k, int64_t splits) {
     return p;
 }
 
-// Estimated time: rounds of resident workgroups, each a fixed cost plus its
-// chunks at the shape's rate, plus for split-K a second launch and the
-// partial sums' round trip through memory.
+// Estimated time: full rounds of resident workgroups at the shape's rate,
+// then a partial round whose workgroups share compute units with fewer
+// others (faster each, slower in total), plus for split-K a second launch
+// and the partial sums' round trip through memory.
 double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t batch) {
     const int64_t bk = pamk::kChunkK * c.kw;
     const int64_t chunks = ceil_div(p.k_per_split, bk);
     const int64_t wgs = ceil_div(m, c.bm) * ceil_div(n, c.bn) * batch * p.splits;
-    const int64_t rounds = ceil_div(wgs, (int64_t)c.per_cu * kComputeUnits);
-    const double chunk_s = double(c.bm) * c.bn * bk * c.per_cu * kComputeUnits / c.rate;
-    double t = double(rounds) * (kWorkgroupFixedS + double(chunks) * chunk_s);
+    const int64_t slots = (int64_t)c.per_cu * kComputeUnits;
+    const double wg_s = double(c.bm) * c.bn * bk * chunks * slots / c.rate + kWorkgroupFixedS;
+    const int64_t rounds = wgs / slots;
+    const int64_t rest = wgs % slots;
+    double t = double(rounds) * wg_s;
+    if (rest > 0) {
+        const int q = (int)ceil_div(rest, kComputeUnits);
+        const double partial = wg_s * (double(q) / c.per_cu) * cu_efficiency(c.per_cu * c.waves) /
+                               cu_efficiency(q * c.waves);
+        const double even = wg_s * double(rest) / double(slots);
+        t += even + (partial - even) / (1.0 + kTailDamping * double(rounds));
+    }
     if (p.splits > 1)
         t += kSplitFixedS + double(p.splits + 1) * double(m) * double(n) * double(batch) * 4.0 / kPartialBytesPerS;
     return t;
@@ -87,22 +119,27 @@ double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t ba
 // The cheapest (shape, split) by plan_time; splits keep at least four
 // chunks each.
 Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch) {
-    double best_t = 0.0;
-    Plan best{};
-    bool have = false;
+    double best_t[2] = {0.0, 0.0};
+    Plan best[2] = {};
+    bool have[2] = {false, false};
     for (const auto &c : kShapes) {
         const int64_t most = std::max<int64_t>(1, std::min(kMaxSplits, k / (4 * pamk::kChunkK * c.kw)));
-        for (int64_t s = 1; s <= most; s *= 2) {
+        for (const int s : kSplitChoices) {
+            if (s > most)
+                break;
             const Plan p = make_plan(c, k, s);
             const double t = plan_time(c, p, m, n, batch);
-            if (!have || t < best_t) {
-                best_t = t;
-                best = p;
-                have = true;
+            const int split = p.splits > 1 ? 1 : 0;
+            if (!have[split] || t < best_t[split]) {
+                best_t[split] = t;
+                best[split] = p;
+                have[split] = true;
             }
         }
     }
-    return best;
+    if (have[1] && best_t[1] < kSplitMargin * best_t[0])
+        return best[1];
+    return best[0];
 }
 
 pam_status_t validate(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,

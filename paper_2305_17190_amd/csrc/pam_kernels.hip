@@ -384,13 +384,18 @@ __device__ __forceinline__ void lds_frag(const uint32_t (*s)[BK][LD], int plane,
     out[4] = hi.x; out[5] = hi.y; out[6] = hi.z; out[7] = hi.w;
 }
 
+// Waves each SIMD holds for a tile shape (the register budget per wave is
+// 512 / waves): three for the 128 x 128 tile, whose loop fits 168 registers;
+// two for the smaller tiles, which stage more operand registers per thread.
+constexpr int gemm_waves_per_simd(int bm, int bn, int kw) { return (bm == 128 && bn == 128 && kw == 1) ? 3 : 2; }
+
 // One workgroup computes a BM x BN output tile.  Each of its KW k-groups
 // holds the whole tile in 8 x 8 register micro-tiles (BM * BN / 64 threads)
 // and takes 16 of the 16 * KW k steps of every LDS chunk; with KW > 1 the
 // groups' partial tiles are added through LDS at the end, so small outputs
 // get more waves without extra HBM traffic.
 template <int BM, int BN, int KW, bool TA, bool TB>
-__global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_simd(BM, BN, KW))))
 pam_gemm_kernel(GemmParams p) {
     constexpr int KPG = kChunkK;           // k steps per group per chunk
     constexpr int BK = KPG * KW;           // chunk depth
@@ -494,54 +499,50 @@ pam_gemm_kernel(GemmParams p) {
 
         const uint32_t (*cA)[BK][LDA] = sA;
         const uint32_t (*cB)[BK][LDB] = sB;
-        if (!special) {
-            // Accumulation order is free, so a wave runs its S2 k steps first
-            // and its S3 k steps after them; neither loop body branches.
-            auto s2_step = [&](int kk) {
-                uint32_t am[8], mm[8], bb[8];
-                lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
-                lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
-                lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
+        // The wave's k steps of this chunk as three bit sets, taken by three
+        // loops in sequence (accumulation order is free): S2 steps, S3 steps,
+        // and for a SPECIAL chunk every step with the complete definition.
+        // Loops in sequence, rather than alternative paths, keep the
+        // accumulator tile in one set of registers.
+        const uint32_t s2_bits = special ? 0u : (~slow & 0xFFFFu);
+        const uint32_t s3_bits = special ? 0u : slow;
+        const uint32_t sp_bits = special ? 0xFFFFu : 0u;
+        for (uint32_t todo = s2_bits; todo != 0u; todo &= todo - 1u) {
+            const int kk = k_first + __builtin_ctz(todo);
+            uint32_t am[8], mm[8], bb[8];
+            lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
+            lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
+            lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
 #pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    s2_row(acc[i], am[i], mm[i], bb);
-            };
-            if (slow == 0u) {
+            for (int i = 0; i < 8; ++i)
+                s2_row(acc[i], am[i], mm[i], bb);
+        }
+        for (uint32_t todo = s3_bits; todo != 0u; todo &= todo - 1u) {
+            const int kk = k_first + __builtin_ctz(todo);
+            uint32_t am[8], mm[8], bb[8];
+            lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
+            lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
+            lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
 #pragma unroll
-                for (int j = 0; j < KPG; ++j)
-                    s2_step(k_first + j);
-            } else {
-                for (uint32_t todo = ~slow & 0xFFFFu; todo != 0u; todo &= todo - 1u)
-                    s2_step(k_first + __builtin_ctz(todo));
-                for (uint32_t todo = slow; todo != 0u; todo &= todo - 1u) {
-                    const int kk = k_first + __builtin_ctz(todo);
-                    uint32_t am[8], mm[8], bb[8];
-                    lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
-                    lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
-                    lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
-#pragma unroll
-                    for (int i = 0; i < 8; ++i)
-                        s3_row(acc[i], am[i], mm[i], bb);
-                }
-            }
-        } else {
-            // SPECIAL: rebuild each operand's encoding (A: sign and exponent
-            // from m, mantissa from aM; B: b' + bias, denormals already zero)
-            // and apply the complete definition per MAC.
+            for (int i = 0; i < 8; ++i)
+                s3_row(acc[i], am[i], mm[i], bb);
+        }
+        // SPECIAL: rebuild each operand's encoding (A: sign and exponent from
+        // m, mantissa from aM; B: b' + bias, denormals already zero) and
+        // apply the complete definition per MAC.
 #pragma unroll 1
-            for (int j = 0; j < KPG; ++j) {
-                const int kk = k_first + j;
-                uint32_t am[8], mm[8], bb[8];
-                lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
-                lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
-                lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
+        for (uint32_t todo = sp_bits; todo != 0u; todo &= todo - 1u) {
+            const int kk = k_first + __builtin_ctz(todo);
+            uint32_t am[8], mm[8], bb[8];
+            lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
+            lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
+            lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    const uint32_t a = mm[i] | (am[i] & kMant);
+            for (int i = 0; i < 8; ++i) {
+                const uint32_t a = mm[i] | (am[i] & kMant);
 #pragma unroll
-                    for (int j2 = 0; j2 < 8; ++j2)
-                        acc[i][j2] += __uint_as_float(pam_full(a, bb[j2] + kBias));
-                }
+                for (int j = 0; j < 8; ++j)
+                    acc[i][j] += __uint_as_float(pam_full(a, bb[j] + kBias));
             }
         }
     }

@@ -75,10 +75,15 @@ def test_empty_products_launch_nothing(lib):
 
 
 def test_plan_selection_is_host_logic(lib):
-    # Large products use the 128x128 tile without split-K.
+    # Large products use the 128x128 tile (three workgroups per compute
+    # unit, 768 slots); with 4096 tiles the last partial round is cheap and
+    # K stays whole.
     assert pam.plan(16384, 4096, 4096) == (128, 128, 1, 1)
-    assert pam.plan(4096, 4096, 16384) == (128, 128, 1, 1)
-    assert pam.plan(8192, 2048, 512) == (128, 128, 1, 1)
+    # 1024 tiles on 768 slots would leave a last round on a third of the
+    # slots: K is split so the workgroups fill whole rounds.
+    tm, tn, s, kg = pam.plan(4096, 4096, 16384)
+    assert (tm, tn, kg) == (128, 128, 1) and 2 <= s <= 8
+    assert pam.plan(8192, 2048, 512)[:2] == (128, 128)
     # Narrow outputs with long K split K; short-K batched narrow outputs use
     # the 64x64 tile whose four waves share each chunk's k steps.
     assert pam.plan(8192, 512, 2048)[2] > 1

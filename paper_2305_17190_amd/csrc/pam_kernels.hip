@@ -273,7 +273,12 @@ struct TileLoader {
             for (int c = 0; c < 4; ++c) {
                 const uint32_t u = e[c];
                 if (is_b) {
-                    p0[c] = (((u & kExpMask) == 0u) ? (u & kSign) : u) - kBias;
+                    // Multiplying by 1.0 flushes a denormal to the signed
+                    // zero (denormals are flushed); everything else passes
+                    // unchanged (a NaN stays a NaN).
+                    uint32_t f;
+                    asm("v_mul_f32 %0, 1.0, %1" : "=v"(f) : "v"(u));
+                    p0[c] = f - kBias;
                     p1[c] = 0u;
                 } else {
                     p0[c] = (u & kMant) | kBias;

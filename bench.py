@@ -106,30 +106,48 @@ def cpu_baseline(workload_id: int, host, forms, target_s: float) -> dict:
     }
 
 
+ELEMENTWISE_OPS = {
+    # op: (binding name, kernel, bytes per element, input description)
+    "mul": ("mul", "pam_mul_vec4_kernel", 12, "N(0,1) with 1% zeros and 1% powers of two"),
+    "pad": ("pad", "binary_vec4_kernel<PadOp>", 12, "N(0,1) with 1% zeros and 1% powers of two"),
+    "palog2": ("palog2", "unary_vec4_kernel<Palog2Op>", 8, "|N(0,1)| with 1% zeros and 1% powers of two"),
+    "paexp2": ("paexp2", "unary_vec4_kernel<Paexp2Op>", 8, "softmax-shaped arguments"),
+}
+
+
 def bench_elementwise(args, torch, wl, pam, dev) -> int:
-    """pam_mul on N elements: 8 bytes read and 4 written per element."""
+    """One elementwise op on N elements: 8 bytes read and 4 written per element
+    (two-operand ops), or 4 read and 4 written (one-operand ops)."""
     n = args.elementwise
-    a, b = wl.pam_mul_inputs(n, 1000 + 3)
-    da, db = torch.from_numpy(a).to(dev), torch.from_numpy(b).to(dev)
-    out = torch.empty_like(da)
+    name, kernel, nbytes, desc = ELEMENTWISE_OPS[args.elementwise_op]
+    fn = getattr(pam, name)
+    if args.elementwise_op == "paexp2":
+        a = wl.paexp2_arguments(n, 1000 + 4)
+        ins = (torch.from_numpy(a).to(dev),)
+    else:
+        a, b = wl.pam_mul_inputs(n, 1000 + 3)
+        ins = (torch.from_numpy(a).to(dev), torch.from_numpy(b).to(dev))
+        if args.elementwise_op == "palog2":
+            ins = (ins[0].abs(),)
+    out = torch.empty_like(ins[0])
     for _ in range(args.warmup):
-        pam.mul(da, db, out=out)
+        fn(*ins, out=out)
     torch.cuda.synchronize()
     s = torch.cuda.Event(enable_timing=True)
     e = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     s.record()
     for _ in range(args.steps):
-        pam.mul(da, db, out=out)
+        fn(*ins, out=out)
     e.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     launch_s = s.elapsed_time(e) / 1e3 / args.steps
-    gbs = 12.0 * n / launch_s / 1e9
+    gbs = float(nbytes) * n / launch_s / 1e9
     result = {
-        "metric": "elementwise pam_mul throughput",
+        "metric": f"elementwise {args.elementwise_op} throughput",
         "value": round(n / launch_s / 1e9, 3),
-        "unit": "G PAM/s",
+        "unit": "G elements/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -139,10 +157,10 @@ def bench_elementwise(args, torch, wl, pam, dev) -> int:
         "vs_baseline": None,
         "dtype": "u32",
         "data": "synthetic",
-        "config": {"workload": f"pam_mul n={n}, N(0,1) with 1% zeros and 1% powers of two"},
-        "roofline": {"bound": "hbm", "kernel": "pam_mul_vec4_kernel", "achieved": round(gbs, 1),
+        "config": {"workload": f"{args.elementwise_op} n={n}, {desc}"},
+        "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(gbs, 1),
                      "peak": 8000.0, "unit": "GB/s", "frac": round(gbs / 8000.0, 4), "traffic": None,
-                     "bytes_per_element": 12, "avg_launch_ms": round(launch_s * 1e3, 5)},
+                     "bytes_per_element": nbytes, "avg_launch_ms": round(launch_s * 1e3, 5)},
     }
     print(json.dumps(result), flush=True)
     return 0
@@ -159,7 +177,9 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy (reference kernel for HBM counters)")
     ap.add_argument("--elementwise", type=int, default=0, metavar="N",
-                    help="time only elementwise pam_mul on N elements (HBM roofline) and print its line")
+                    help="time only one elementwise op on N elements (HBM roofline) and print its line")
+    ap.add_argument("--elementwise-op", default="mul", choices=sorted(ELEMENTWISE_OPS),
+                    help="the elementwise op --elementwise times (default mul)")
     args = ap.parse_args()
 
     if args.gpus != 1:

@@ -74,6 +74,36 @@ typedef enum { PAM_OP_N = 0, PAM_OP_T = 1 } pam_op_t;
 pam_status_t pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
 
 /*
+ * Elementwise piecewise affine division (PAD, Sec. 2.3), the inverse of PAM:
+ * out[i] = a[i] ./ b[i], the int32 difference of the encodings plus one
+ * exponent bias (127 << 23), whose borrow realises 1{M_A - M_B < 0} (the
+ * printed exponent / mantissa lines of Sec. 2.3 are read with this borrow).
+ * Sign = exclusive or; denormal operands count as zero; a NaN operand,
+ * 0 ./ 0 and inf ./ inf give 0x7FC00000; x ./ 0 and inf ./ x give a signed
+ * inf; 0 ./ x and x ./ inf a signed zero; a result exponent field <= 0 a
+ * signed zero, >= 255 +-FLT_MAX.  Bit-exact: one result per operand pair.
+ * a, b, out: device arrays of n float32 (out may alias a or b); n >= 0.
+ */
+pam_status_t pam_pad(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
+
+/*
+ * Elementwise palog2 (Sec. 2.3): out[i] = E + M for a[i] = 2^E (1 + M) > 0,
+ * rounded to the nearest float32 (ties to even).  +-0 and denormals give
+ * -inf, negative inputs NaN (0x7FC00000), +inf +inf, NaN 0x7FC00000.
+ * a, out: device arrays of n float32 (out may alias a); n >= 0.
+ */
+pam_status_t pam_palog2(const float *a, float *out, int64_t n, hipStream_t stream);
+
+/*
+ * Elementwise paexp2 (Sec. 2.3): out[i] = 2^floor(x) (1 + x - floor(x)) for
+ * x = a[i], rounded to the nearest float32 (ties to even).  Results below
+ * 2^-126 are +0, above FLT_MAX +inf; -inf gives +0, NaN 0x7FC00000;
+ * denormal inputs count as zero.  a, out: device arrays of n float32 (out
+ * may alias a); n >= 0.
+ */
+pam_status_t pam_paexp2(const float *a, float *out, int64_t n, hipStream_t stream);
+
+/*
  * PAM matrix product (Sec. 3.2): C(i, j) = sum_p op(A)(i, p) .^ op(B)(p, j)
  * for 0 <= i < m, 0 <= j < n, float32 accumulation.
  * The forward pass of a linear layer Y = X W^T is (N, T); its approximate

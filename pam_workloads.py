@@ -95,6 +95,22 @@ def pam_mul_inputs(n: int, seed: int) -> Tuple[np.ndarray, np.ndarray]:
     return out[0], out[1]
 
 
+def paexp2_arguments(n: int, seed: int) -> np.ndarray:
+    """Arguments of paexp2 as piecewise affine softmax and exp produce them:
+    half x - max(x) of N(0, 4^2) logits (mostly in [-30, 0]), a quarter
+    U(-140, 140) (both saturations), a quarter small |x| < 1 of random
+    exponents (where the result needs rounding)."""
+    g = rng(seed)
+    h, q = n // 2, n // 4
+    logits = (4.0 * g.standard_normal(size=h)).astype(np.float32)
+    a = (logits - logits.max()).astype(np.float32) if h else logits
+    b = g.uniform(-140.0, 140.0, size=q).astype(np.float32)
+    c_bits = ((g.integers(0, 2, size=n - h - q) << 31) | (g.integers(60, 127, size=n - h - q) << 23)
+              | g.integers(0, 1 << 23, size=n - h - q)).astype(np.uint32)
+    x = np.concatenate([a, b, c_bits.view(np.float32)])
+    return x[g.permutation(n)]
+
+
 def random_bit_patterns(n: int, seed: int) -> np.ndarray:
     """Uniformly random 32-bit patterns viewed as float32 (all classes)."""
     return rng(seed).integers(0, 1 << 32, size=n, dtype=np.uint64).astype(np.uint32).view(np.float32)

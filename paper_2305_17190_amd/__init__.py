@@ -7,6 +7,8 @@ stream.  There is no CPU fallback; without the built library or a gfx950
 device every call raises.
 
     mul(a, b, out=None)                        elementwise a .^ b
+    pad(a, b, out=None)                        elementwise a ./ b (Sec. 2.3)
+    palog2(a, out=None), paexp2(a, out=None)   elementwise (Sec. 2.3)
     gemm(A, B, trans_a, trans_b, out=None)     C = op(A) .^ op(B)
     bmm(A, B, trans_a, trans_b, out=None)      batched over the leading axis
 
@@ -22,7 +24,8 @@ import ctypes
 import os
 from typing import Optional
 
-__all__ = ["mul", "gemm", "bmm", "plan", "device_info", "library_path", "load", "PamError"]
+__all__ = ["mul", "pad", "palog2", "paexp2", "gemm", "bmm", "plan", "device_info", "library_path", "load",
+           "PamError"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpam.so")
@@ -49,8 +52,8 @@ class _DeviceInfo(ctypes.Structure):
 _lib = None
 
 # Every symbol include/pam.h declares.
-EXPORTS = ("pam_mul", "pam_gemm", "pam_gemm_batched", "pam_gemm_plan", "pam_gemm_batched_with_plan",
-           "pam_device_info", "pam_status_string", "pam_last_error")
+EXPORTS = ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_gemm", "pam_gemm_batched", "pam_gemm_plan",
+           "pam_gemm_batched_with_plan", "pam_device_info", "pam_status_string", "pam_last_error")
 
 
 def library_path() -> str:
@@ -67,14 +70,17 @@ def load() -> ctypes.CDLL:
     lib = ctypes.CDLL(LIB_PATH)
     i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
     lib.pam_mul.argtypes = [vp, vp, vp, i64, vp]
+    lib.pam_pad.argtypes = [vp, vp, vp, i64, vp]
+    lib.pam_palog2.argtypes = [vp, vp, i64, vp]
+    lib.pam_paexp2.argtypes = [vp, vp, i64, vp]
     lib.pam_gemm.argtypes = [i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp]
     lib.pam_gemm_batched.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, vp]
     lib.pam_gemm_batched_with_plan.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64,
                                                i64, ctypes.POINTER(_Plan), vp]
     lib.pam_gemm_plan.argtypes = [i64, i64, i64, i64, ctypes.POINTER(_Plan)]
     lib.pam_device_info.argtypes = [i32, ctypes.POINTER(_DeviceInfo)]
-    for name in ("pam_mul", "pam_gemm", "pam_gemm_batched", "pam_gemm_batched_with_plan", "pam_gemm_plan",
-                 "pam_device_info"):
+    for name in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_gemm", "pam_gemm_batched",
+                 "pam_gemm_batched_with_plan", "pam_gemm_plan", "pam_device_info"):
         getattr(lib, name).restype = i32
     lib.pam_status_string.argtypes = [i32]
     lib.pam_status_string.restype = ctypes.c_char_p
@@ -114,20 +120,49 @@ def _require(t, name: str, ndim: int):
         raise ValueError(f"{name} must have a contiguous last dimension")
 
 
-def mul(a, b, out=None):
-    """Elementwise PAM of two equally shaped contiguous float32 tensors."""
+def _elementwise_args(tensors, out):
     torch = _torch()
-    for name, t in (("a", a), ("b", b)):
+    for name, t in tensors:
         _require(t, name, t.dim() if isinstance(t, torch.Tensor) else 1)
         if not t.is_contiguous():
             raise ValueError(f"{name} must be contiguous")
-    if a.shape != b.shape:
-        raise ValueError(f"shape mismatch {tuple(a.shape)} vs {tuple(b.shape)}")
+    a = tensors[0][1]
+    for name, t in tensors[1:]:
+        if t.shape != a.shape:
+            raise ValueError(f"shape mismatch {tuple(a.shape)} vs {tuple(t.shape)}")
     if out is None:
         out = torch.empty_like(a)
-    elif out.shape != a.shape or not out.is_contiguous() or out.dtype != torch.float32:
-        raise ValueError("out must be a contiguous float32 tensor of the same shape")
+    elif (not isinstance(out, torch.Tensor) or out.shape != a.shape or not out.is_contiguous()
+          or out.dtype != torch.float32 or out.device != a.device):
+        raise ValueError("out must be a contiguous float32 tensor of the same shape and device")
+    return a, out
+
+
+def mul(a, b, out=None):
+    """Elementwise PAM of two equally shaped contiguous float32 tensors."""
+    a, out = _elementwise_args((("a", a), ("b", b)), out)
     _check(load().pam_mul(a.data_ptr(), b.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
+    return out
+
+
+def pad(a, b, out=None):
+    """Elementwise piecewise affine division a ./ b (Sec. 2.3)."""
+    a, out = _elementwise_args((("a", a), ("b", b)), out)
+    _check(load().pam_pad(a.data_ptr(), b.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
+    return out
+
+
+def palog2(a, out=None):
+    """Elementwise palog2(a) = E + M (Sec. 2.3), rounded to float32."""
+    a, out = _elementwise_args((("a", a),), out)
+    _check(load().pam_palog2(a.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
+    return out
+
+
+def paexp2(a, out=None):
+    """Elementwise paexp2(a) = 2^floor(a) (1 + a - floor(a)) (Sec. 2.3), rounded to float32."""
+    a, out = _elementwise_args((("a", a),), out)
+    _check(load().pam_paexp2(a.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
     return out
 
 

@@ -326,6 +326,54 @@ pam_status_t pam_mul(const float *a, const float *b, float *out, int64_t n, hipS
     return PAM_SUCCESS;
 }
 
+pam_status_t pam_pad(const float *a, const float *b, float *out, int64_t n, hipStream_t stream) {
+    if (n < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "n must be >= 0");
+    if (n == 0)
+        return PAM_SUCCESS;
+    if (a == nullptr || b == nullptr || out == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "a, b and out must be non-NULL");
+    pam_status_t st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    hipError_t e = pamk::launch_pad(a, b, out, n, stream);
+    if (e != hipSuccess)
+        return fail_hip(e, "pam_pad kernel launch");
+    return PAM_SUCCESS;
+}
+
+pam_status_t pam_palog2(const float *a, float *out, int64_t n, hipStream_t stream) {
+    if (n < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "n must be >= 0");
+    if (n == 0)
+        return PAM_SUCCESS;
+    if (a == nullptr || out == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "a and out must be non-NULL");
+    pam_status_t st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    hipError_t e = pamk::launch_palog2(a, out, n, stream);
+    if (e != hipSuccess)
+        return fail_hip(e, "pam_palog2 kernel launch");
+    return PAM_SUCCESS;
+}
+
+pam_status_t pam_paexp2(const float *a, float *out, int64_t n, hipStream_t stream) {
+    if (n < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "n must be >= 0");
+    if (n == 0)
+        return PAM_SUCCESS;
+    if (a == nullptr || out == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "a and out must be non-NULL");
+    pam_status_t st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    hipError_t e = pamk::launch_paexp2(a, out, n, stream);
+    if (e != hipSuccess)
+        return fail_hip(e, "pam_paexp2 kernel launch");
+    return PAM_SUCCESS;
+}
+
 pam_status_t pam_gemm(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                       const float *B, int64_t ldb, float *C, int64_t ldc, hipStream_t stream) {
     pam_status_t st = validate(transA, transB, m, n, k, A, lda, 0, B, ldb, 0, C, ldc, 0, 1);

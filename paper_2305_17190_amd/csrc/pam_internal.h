@@ -29,6 +29,11 @@ struct GemmParams {
 
 hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
 
+// Elementwise PAD, palog2 and paexp2 (pa_ops.hip).
+hipError_t launch_pad(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
+hipError_t launch_palog2(const float *a, float *out, int64_t n, hipStream_t stream);
+hipError_t launch_paexp2(const float *a, float *out, int64_t n, hipStream_t stream);
+
 // (tile_m, tile_n, kgroups) in {(128,128,1), (128,64,1), (64,64,1), (64,64,4)};
 // grid = (tiles_m * tiles_n, splits, batch_in_launch).
 hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b,

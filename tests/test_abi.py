@@ -14,7 +14,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(pam_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(pam_[a-z_0-9]+)\s*\(", text)))
 
 
 @pytest.fixture(scope="module")
@@ -26,7 +26,8 @@ def lib():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for want in ("pam_mul", "pam_gemm", "pam_gemm_batched", "pam_status_string", "pam_last_error"):
+    for want in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_gemm", "pam_gemm_batched",
+                 "pam_status_string", "pam_last_error"):
         assert want in names
 
 
@@ -72,6 +73,18 @@ def test_empty_products_launch_nothing(lib):
     assert lib.pam_gemm_batched(0, 0, 4, 4, 4, None, 4, 0, None, 4, 0, None, 4, 0, 0, None) == 0
     assert lib.pam_mul(None, None, None, 0, None) == 0
     assert lib.pam_mul(None, None, None, -1, None) == 1
+    assert lib.pam_pad(None, None, None, 0, None) == 0
+    assert lib.pam_pad(None, None, None, -1, None) == 1
+    assert lib.pam_palog2(None, None, 0, None) == 0
+    assert lib.pam_paexp2(None, None, -2, None) == 1
+
+
+def test_elementwise_rejects_null_pointers(lib):
+    assert lib.pam_mul(None, 8, 8, 4, None) == 1
+    assert lib.pam_pad(8, None, 8, 4, None) == 1
+    assert lib.pam_palog2(8, None, 4, None) == 1
+    assert lib.pam_paexp2(None, 8, 4, None) == 1
+    assert lib.pam_last_error() != b""
 
 
 def test_plan_selection_is_host_logic(lib):
@@ -117,3 +130,8 @@ def test_binding_refuses_cpu_tensors():
         pam.mul(a, a)
     with pytest.raises(pam.PamError):
         pam.gemm(torch.ones(2, 2), torch.ones(2, 2))
+    for fn in (pam.palog2, pam.paexp2):
+        with pytest.raises(pam.PamError):
+            fn(a)
+    with pytest.raises(pam.PamError):
+        pam.pad(a, a)

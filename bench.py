@@ -166,6 +166,64 @@ def bench_elementwise(args, torch, wl, pam, dev) -> int:
     return 0
 
 
+def bench_autograd(args, torch, wl, pam, dev) -> int:
+    """One PAM linear layer through autograd: forward Y = X .^ W^T, then
+    backward with the approximate derivative (dX = dY .^ W, dW = dY^T .^ X)
+    on the workload's tensors -- the same three products as the default step,
+    plus the wrapper's own work."""
+    from paper_2305_17190_amd.autograd import pam_linear
+
+    wid = int(args.workload[1:])
+    spec = wl.WORKLOADS[wid]
+    names = [f.name for f in spec["forms"]]
+    if names != ["fwd", "dX", "dW"]:
+        print(f"--autograd needs a single-linear-layer workload (w2 or w5), not {args.workload}", file=sys.stderr)
+        return 2
+    host = wl.workload_inputs(wid)
+    x = torch.from_numpy(host["X"]).to(dev).requires_grad_()
+    w = torch.from_numpy(host["W"]).to(dev).requires_grad_()
+    dy = torch.from_numpy(host["dY"]).to(dev)
+    macs = sum(f.macs for f in spec["forms"])
+
+    def step():
+        x.grad = None
+        w.grad = None
+        pam_linear(x, w).backward(dy)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    s.record()
+    for _ in range(args.steps):
+        step()
+    e.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    step_s = s.elapsed_time(e) / 1e3 / args.steps
+    log(f"autograd step {step_s * 1e3:.3f} ms ({macs / step_s / 1e9:.1f} GPAM-MAC/s)")
+    result = {
+        "metric": "PAM linear layer forward + backward through autograd, G PAM-MAC/s",
+        "value": round(macs / step_s / 1e9, 3),
+        "unit": "GPAM-MAC/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": spec["name"], "layer": "paper_2305_17190_amd.autograd.pam_linear, no bias",
+                   "pam_macs_per_step": macs},
+    }
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -178,6 +236,8 @@ def main() -> int:
                     help="only run a plain 1 GiB device-to-device copy (reference kernel for HBM counters)")
     ap.add_argument("--elementwise", type=int, default=0, metavar="N",
                     help="time only one elementwise op on N elements (HBM roofline) and print its line")
+    ap.add_argument("--autograd", action="store_true",
+                    help="time one PAM linear layer forward + backward through autograd (w2, w5)")
     ap.add_argument("--elementwise-op", default="mul", choices=sorted(ELEMENTWISE_OPS),
                     help="the elementwise op --elementwise times (default mul)")
     args = ap.parse_args()
@@ -208,6 +268,8 @@ def main() -> int:
     pam.load()
     if args.elementwise:
         return bench_elementwise(args, torch, wl, pam, dev)
+    if args.autograd:
+        return bench_autograd(args, torch, wl, pam, dev)
 
     wid = int(args.workload[1:])
     spec = wl.WORKLOADS[wid]

@@ -135,3 +135,13 @@ def test_binding_refuses_cpu_tensors():
             fn(a)
     with pytest.raises(pam.PamError):
         pam.pad(a, a)
+
+
+def test_autograd_wrappers_refuse_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    from paper_2305_17190_amd.autograd import PAMLinear, pam_matmul
+    lin = PAMLinear(4, 3)
+    with pytest.raises(pam.PamError):
+        lin(torch.ones(2, 4))
+    with pytest.raises(pam.PamError):
+        pam_matmul(torch.ones(2, 2), torch.ones(2, 2))

@@ -43,6 +43,14 @@ in the HIP library):
       this oracle accumulates in float64 in increasing k, and also returns
       S = sum_k |term| so that callers can bound float32 rounding.
 
+  R11 narrower mantissas (App. "PAM with Narrower Mantissas": inputs are
+      rounded and their extra mantissa bits masked, accumulation unchanged):
+      each input is rounded to the nearest float32 whose mantissa has m
+      significant bits (ties to even), a carry moving into the exponent and
+      a finite value rounding past FLT_MAX becoming inf, as a narrower
+      float format's conversion does; inf stays inf and NaN stays NaN.  The
+      rounded inputs then go through PAM (R1-R7) with float32 accumulation.
+
 Three independent renderings of the scalar product are given (bit, field and
 value form); the tests check them against each other and against the facts
 the paper states.
@@ -178,6 +186,74 @@ def pam_mul_ref(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     out = np.where(a_inf | b_inf, inf_res, out)               # R6
     out = np.where((ma > INF) | (mb > INF), QNAN, out)        # R6
     return out.astype(np.uint32).view(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# Narrower mantissas (R11)
+# ---------------------------------------------------------------------------
+
+def round_mantissa_bits(u: int, bits: int) -> int:
+    """One float32 encoding rounded to ``bits`` mantissa bits (R11), scalar form.
+
+    Works on the value: decode, round the significand 1.M (or 0.M for a
+    denormal) to a multiple of 2^-bits with ties to even, re-encode.
+    """
+    s, ex, fr = u >> 31, (u >> 23) & 0xFF, u & 0x7FFFFF
+    if ex == 255:
+        return u
+    drop = 23 - bits
+    if drop == 0:
+        return u
+    sig = fr | ((1 << 23) if ex else 0)            # 24-bit significand (23 for denormals)
+    q, r = divmod(sig, 1 << drop)
+    half = 1 << (drop - 1)
+    if r > half or (r == half and (q & 1)):
+        q += 1
+    sig = q << drop
+    e = ex if ex else 1
+    if sig >= (1 << 24):                            # carry out of the significand
+        sig >>= 1
+        e += 1
+    if ex == 0 and sig >= (1 << 23):                # a denormal rounded up to the min normal
+        e, sig = 1, sig
+        return (s << 31) | (1 << 23) | (sig - (1 << 23))
+    if ex == 0:
+        return (s << 31) | sig
+    if e >= 255:
+        return (s << 31) | INF
+    return (s << 31) | (e << 23) | (sig - (1 << 23))
+
+
+def round_mantissa_scalar_ref(x: np.ndarray, bits: int) -> np.ndarray:
+    """Elementwise R11 rounding through the scalar value form (slow)."""
+    x = np.asarray(x, dtype=np.float32)
+    u = x.view(np.uint32).reshape(-1)
+    out = np.fromiter((round_mantissa_bits(int(v), bits) for v in u), dtype=np.uint32, count=u.size)
+    return out.view(np.float32).reshape(x.shape)
+
+
+def round_mantissa_ref(x: np.ndarray, bits: int) -> np.ndarray:
+    """Elementwise R11 rounding of a float32 array to ``bits`` mantissa bits.
+
+    On the encoding: the dropped low bits decide the rounding (above half, or
+    exactly half with an odd kept part, rounds the kept part up); a carry out
+    of the mantissa moves into the exponent, and past the largest exponent
+    lands on the inf encoding.  inf and NaN encodings are left as they are.
+    """
+    if not 0 <= bits <= 23:
+        raise ValueError("bits must be in [0, 23]")
+    x = np.asarray(x, dtype=np.float32)
+    if bits == 23:
+        return x.copy()
+    u = x.view(np.uint32).astype(np.int64)
+    drop = 23 - bits
+    low = u & ((1 << drop) - 1)
+    kept = u >> drop
+    half = 1 << (drop - 1)
+    up = (low > half) | ((low == half) & ((kept & 1) == 1))
+    r = (kept + up.astype(np.int64)) << drop                 # may carry into the exponent (and up to inf)
+    r = np.where((u & INF) == INF, u, r)
+    return r.astype(np.uint32).view(np.float32)
 
 
 # ---------------------------------------------------------------------------

@@ -236,6 +236,8 @@ def main() -> int:
                     help="only run a plain 1 GiB device-to-device copy (reference kernel for HBM counters)")
     ap.add_argument("--elementwise", type=int, default=0, metavar="N",
                     help="time only one elementwise op on N elements (HBM roofline) and print its line")
+    ap.add_argument("--mantissa-bits", type=int, default=23,
+                    help="round every operand to this many mantissa bits first (narrow products; default 23 = none)")
     ap.add_argument("--autograd", action="store_true",
                     help="time one PAM linear layer forward + backward through autograd (w2, w5)")
     ap.add_argument("--elementwise-op", default="mul", choices=sorted(ELEMENTWISE_OPS),
@@ -284,9 +286,11 @@ def main() -> int:
 
     def launch(f):
         if f.batch > 1:
-            pam.bmm(dt[f.a], dt[f.b], trans_a=f.trans_a, trans_b=f.trans_b, out=outs[f.name])
+            pam.bmm(dt[f.a], dt[f.b], trans_a=f.trans_a, trans_b=f.trans_b, out=outs[f.name],
+                    mantissa_bits=args.mantissa_bits)
         else:
-            pam.gemm(dt[f.a], dt[f.b], trans_a=f.trans_a, trans_b=f.trans_b, out=outs[f.name])
+            pam.gemm(dt[f.a], dt[f.b], trans_a=f.trans_a, trans_b=f.trans_b, out=outs[f.name],
+                     mantissa_bits=args.mantissa_bits)
 
     macs_per_step = sum(f.macs for f in forms)
     for _ in range(args.warmup):
@@ -345,6 +349,7 @@ def main() -> int:
                          f"{f.batch}x{f.m}x{f.n}x{f.k}" for f in forms],
             "pam_macs_per_step": macs_per_step,
             "parallelism": "single GPU",
+            **({"mantissa_bits": args.mantissa_bits} if args.mantissa_bits != 23 else {}),
         },
         "roofline": {
             "bound": "alu",

@@ -162,6 +162,30 @@ pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB,
                                         hipStream_t stream);
 
 /*
+ * Narrower-mantissa PAM matrix products (App. "PAM with Narrower
+ * Mantissas"): every element of op(A) and op(B) is first rounded to
+ * `mantissa_bits` mantissa bits (nearest, ties to even; a carry moves into
+ * the exponent, a finite value rounding past FLT_MAX becomes inf; inf and
+ * NaN unchanged), then multiplied with PAM and accumulated in float32 as in
+ * pam_gemm_batched.  The caller's A and B are not modified.  mantissa_bits in
+ * [0, 23] (23 = pam_gemm_batched); arguments otherwise as pam_gemm_batched.
+ */
+pam_status_t pam_gemm_narrow(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                             const float *A, int64_t lda, int64_t strideA,
+                             const float *B, int64_t ldb, int64_t strideB,
+                             float *C, int64_t ldc, int64_t strideC,
+                             int64_t batch, int32_t mantissa_bits, hipStream_t stream);
+
+/*
+ * The same rounding as an elementwise op: out[i] = a[i] rounded to
+ * `mantissa_bits` mantissa bits (App. "PAM with Narrower Mantissas"), e.g. to
+ * keep narrow copies of weights.  a, out: device arrays of n float32 (out may
+ * alias a); n >= 0; mantissa_bits in [0, 23].
+ */
+pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t mantissa_bits,
+                                hipStream_t stream);
+
+/*
  * Figures of `device` that set the vector-ALU roofline: compute units,
  * SIMDs per compute unit and peak engine clock (kHz) read from the HIP
  * runtime and HSA, wavefront size, and the lanes a SIMD retires per clock

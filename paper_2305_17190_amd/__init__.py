@@ -9,6 +9,7 @@ device every call raises.
     mul(a, b, out=None)                        elementwise a .^ b
     pad(a, b, out=None)                        elementwise a ./ b (Sec. 2.3)
     palog2(a, out=None), paexp2(a, out=None)   elementwise (Sec. 2.3)
+    round_mantissa(a, bits, out=None)          a rounded to `bits` mantissa bits
     gemm(A, B, trans_a, trans_b, out=None)     C = op(A) .^ op(B)
     bmm(A, B, trans_a, trans_b, out=None)      batched over the leading axis
 
@@ -24,8 +25,8 @@ import ctypes
 import os
 from typing import Optional
 
-__all__ = ["mul", "pad", "palog2", "paexp2", "gemm", "bmm", "plan", "device_info", "library_path", "load",
-           "PamError"]
+__all__ = ["mul", "pad", "palog2", "paexp2", "round_mantissa", "gemm", "bmm", "plan", "device_info",
+           "library_path", "load", "PamError"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpam.so")
@@ -52,8 +53,9 @@ class _DeviceInfo(ctypes.Structure):
 _lib = None
 
 # Every symbol include/pam.h declares.
-EXPORTS = ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_gemm", "pam_gemm_batched", "pam_gemm_plan",
-           "pam_gemm_batched_with_plan", "pam_device_info", "pam_status_string", "pam_last_error")
+EXPORTS = ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm", "pam_gemm_batched",
+           "pam_gemm_narrow", "pam_gemm_plan", "pam_gemm_batched_with_plan", "pam_device_info", "pam_status_string",
+           "pam_last_error")
 
 
 def library_path() -> str:
@@ -73,14 +75,17 @@ def load() -> ctypes.CDLL:
     lib.pam_pad.argtypes = [vp, vp, vp, i64, vp]
     lib.pam_palog2.argtypes = [vp, vp, i64, vp]
     lib.pam_paexp2.argtypes = [vp, vp, i64, vp]
+    lib.pam_round_mantissa.argtypes = [vp, vp, i64, i32, vp]
+    lib.pam_gemm_narrow.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i32, vp]
     lib.pam_gemm.argtypes = [i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp]
     lib.pam_gemm_batched.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, vp]
     lib.pam_gemm_batched_with_plan.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64,
                                                i64, ctypes.POINTER(_Plan), vp]
     lib.pam_gemm_plan.argtypes = [i64, i64, i64, i64, ctypes.POINTER(_Plan)]
     lib.pam_device_info.argtypes = [i32, ctypes.POINTER(_DeviceInfo)]
-    for name in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_gemm", "pam_gemm_batched",
-                 "pam_gemm_batched_with_plan", "pam_gemm_plan", "pam_device_info"):
+    for name in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm",
+                 "pam_gemm_batched", "pam_gemm_narrow", "pam_gemm_batched_with_plan", "pam_gemm_plan",
+                 "pam_device_info"):
         getattr(lib, name).restype = i32
     lib.pam_status_string.argtypes = [i32]
     lib.pam_status_string.restype = ctypes.c_char_p
@@ -166,6 +171,13 @@ def paexp2(a, out=None):
     return out
 
 
+def round_mantissa(a, bits: int, out=None):
+    """Elementwise rounding to ``bits`` mantissa bits (App. "PAM with Narrower Mantissas")."""
+    a, out = _elementwise_args((("a", a),), out)
+    _check(load().pam_round_mantissa(a.data_ptr(), out.data_ptr(), a.numel(), int(bits), _stream_handle(a)))
+    return out
+
+
 def _dims(A, B, trans_a: bool, trans_b: bool):
     m, k = (A.shape[-1], A.shape[-2]) if trans_a else (A.shape[-2], A.shape[-1])
     kb, n = (B.shape[-1], B.shape[-2]) if trans_b else (B.shape[-2], B.shape[-1])
@@ -178,8 +190,11 @@ def _ld(t) -> int:
     return max(int(t.stride(-2)), 1) if t.numel() > 0 else max(int(t.shape[-1]), 1)
 
 
-def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None):
-    """C = op(A) .^ op(B) with float32 accumulation; returns C (m x n)."""
+def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, mantissa_bits: int = 23):
+    """C = op(A) .^ op(B) with float32 accumulation; returns C (m x n).
+
+    ``mantissa_bits`` < 23 rounds every operand element to that many mantissa
+    bits first (App. "PAM with Narrower Mantissas")."""
     torch = _torch()
     _require(A, "A", 2)
     _require(B, "B", 2)
@@ -190,17 +205,23 @@ def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None):
         _require(out, "out", 2)
         if tuple(out.shape) != (m, n):
             raise ValueError(f"out must be {m}x{n}")
-    _check(load().pam_gemm(PAM_OP_T if trans_a else PAM_OP_N, PAM_OP_T if trans_b else PAM_OP_N, m, n, k,
-                           A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
-                           _stream_handle(A)))
+    ta = PAM_OP_T if trans_a else PAM_OP_N
+    tb = PAM_OP_T if trans_b else PAM_OP_N
+    if mantissa_bits == 23:
+        _check(load().pam_gemm(ta, tb, m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
+                               _stream_handle(A)))
+    else:
+        _check(load().pam_gemm_narrow(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
+                                      out.data_ptr(), _ld(out), 0, 1, int(mantissa_bits), _stream_handle(A)))
     return out
 
 
-def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None):
+def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None, mantissa_bits: int = 23):
     """Batched C[z] = op(A[z]) .^ op(B[z]) over the leading axis.
 
     ``plan`` = (tile_m, tile_n, splits[, kgroups]) forces a tiling (tests
-    and tuning).
+    and tuning).  ``mantissa_bits`` < 23 rounds every operand element to that
+    many mantissa bits first (the library then picks the plan).
     """
     torch = _torch()
     _require(A, "A", 3)
@@ -220,7 +241,11 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None)
     args = (ta, tb, m, n, k, A.data_ptr(), _ld(A), A.stride(0), B.data_ptr(), _ld(B), B.stride(0),
             out.data_ptr(), _ld(out), out.stride(0), batch)
     lib = load()
-    if plan is None:
+    if mantissa_bits != 23:
+        if plan is not None:
+            raise ValueError("plan and mantissa_bits cannot be combined")
+        _check(lib.pam_gemm_narrow(*args, int(mantissa_bits), _stream_handle(A)))
+    elif plan is None:
         _check(lib.pam_gemm_batched(*args, _stream_handle(A)))
     else:
         p = _Plan(*plan) if len(plan) == 4 else _Plan(plan[0], plan[1], plan[2], 1)

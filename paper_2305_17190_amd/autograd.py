@@ -10,8 +10,11 @@ matrix multiply's gradients are ordinary products.
     C = A .^ B (batched)   dA = dC .^ B^T     dB = A^T .^ dC
 
 Every product runs in the library's HIP kernels (``pam.gemm`` / ``pam.bmm``);
-the bias gradient is an ordinary sum (no multiplication).  Inputs must be
-float32 HIP tensors; there is no CPU path.
+the bias gradient is an ordinary sum (no multiplication).  With
+``mantissa_bits`` < 23 every product, forward and backward, first rounds its
+two operands to that many mantissa bits (App. "PAM with Narrower
+Mantissas"); the tensors themselves are not modified.  Inputs must be float32
+HIP tensors; there is no CPU path.
 """
 from __future__ import annotations
 
@@ -34,12 +37,13 @@ def _last_contiguous(t: torch.Tensor) -> torch.Tensor:
 
 class _PAMLinearFn(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x2d, weight, bias):
+    def forward(ctx, x2d, weight, bias, bits):
         x2d = _last_contiguous(x2d)
         weight = _last_contiguous(weight)
         ctx.save_for_backward(x2d, weight)
         ctx.has_bias = bias is not None
-        y = _gemm(x2d, weight, trans_b=True)                  # Y = X .^ W^T
+        ctx.bits = bits
+        y = _gemm(x2d, weight, trans_b=True, mantissa_bits=bits)   # Y = X .^ W^T
         if bias is not None:
             y += bias
         return y
@@ -50,30 +54,32 @@ class _PAMLinearFn(torch.autograd.Function):
         dy = _last_contiguous(dy)
         dx = dw = db = None
         if ctx.needs_input_grad[0]:
-            dx = _gemm(dy, weight)                            # dX = dY .^ W
+            dx = _gemm(dy, weight, mantissa_bits=ctx.bits)                  # dX = dY .^ W
         if ctx.needs_input_grad[1]:
-            dw = _gemm(dy, x2d, trans_a=True)                 # dW = dY^T .^ X
+            dw = _gemm(dy, x2d, trans_a=True, mantissa_bits=ctx.bits)       # dW = dY^T .^ X
         if ctx.has_bias and ctx.needs_input_grad[2]:
             db = dy.sum(dim=0)
-        return dx, dw, db
+        return dx, dw, db, None
 
 
-def pam_linear(x: torch.Tensor, weight: torch.Tensor, bias: torch.Tensor = None) -> torch.Tensor:
+def pam_linear(x: torch.Tensor, weight: torch.Tensor, bias: torch.Tensor = None,
+               mantissa_bits: int = 23) -> torch.Tensor:
     """``x .^ weight^T + bias`` over the last dimension of x (any leading dims)."""
     if x.dim() < 1:
         raise ValueError("x must have at least one dimension")
     lead = x.shape[:-1]
-    y = _PAMLinearFn.apply(x.reshape(-1, x.shape[-1]), weight, bias)
+    y = _PAMLinearFn.apply(x.reshape(-1, x.shape[-1]), weight, bias, int(mantissa_bits))
     return y.reshape(*lead, weight.shape[0])
 
 
 class _PAMBmmFn(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, a, b):
+    def forward(ctx, a, b, bits):
         a = _last_contiguous(a)
         b = _last_contiguous(b)
         ctx.save_for_backward(a, b)
-        return _bmm(a, b)                                     # C = A .^ B
+        ctx.bits = bits
+        return _bmm(a, b, mantissa_bits=bits)                 # C = A .^ B
 
     @staticmethod
     def backward(ctx, dc):
@@ -81,28 +87,30 @@ class _PAMBmmFn(torch.autograd.Function):
         dc = _last_contiguous(dc)
         da = db = None
         if ctx.needs_input_grad[0]:
-            da = _bmm(dc, b, trans_b=True)                    # dA = dC .^ B^T
+            da = _bmm(dc, b, trans_b=True, mantissa_bits=ctx.bits)     # dA = dC .^ B^T
         if ctx.needs_input_grad[1]:
-            db = _bmm(a, dc, trans_a=True)                    # dB = A^T .^ dC
-        return da, db
+            db = _bmm(a, dc, trans_a=True, mantissa_bits=ctx.bits)     # dB = A^T .^ dC
+        return da, db, None
 
 
-def pam_matmul(a: torch.Tensor, b: torch.Tensor) -> torch.Tensor:
+def pam_matmul(a: torch.Tensor, b: torch.Tensor, mantissa_bits: int = 23) -> torch.Tensor:
     """``a .^ b`` for 2-D or batched 3-D operands (leading batch dimension)."""
     if a.dim() == 2 and b.dim() == 2:
-        return _PAMBmmFn.apply(a.unsqueeze(0), b.unsqueeze(0)).squeeze(0)
+        return _PAMBmmFn.apply(a.unsqueeze(0), b.unsqueeze(0), int(mantissa_bits)).squeeze(0)
     if a.dim() == 3 and b.dim() == 3:
-        return _PAMBmmFn.apply(a, b)
+        return _PAMBmmFn.apply(a, b, int(mantissa_bits))
     raise ValueError("pam_matmul takes two 2-D or two 3-D tensors")
 
 
 class PAMLinear(torch.nn.Module):
     """A linear layer whose products are PAM (forward and approximate-derivative backward)."""
 
-    def __init__(self, in_features: int, out_features: int, bias: bool = True, device=None):
+    def __init__(self, in_features: int, out_features: int, bias: bool = True, device=None,
+                 mantissa_bits: int = 23):
         super().__init__()
         self.in_features = in_features
         self.out_features = out_features
+        self.mantissa_bits = mantissa_bits
         self.weight = torch.nn.Parameter(torch.empty(out_features, in_features, device=device))
         self.bias = torch.nn.Parameter(torch.empty(out_features, device=device)) if bias else None
         self.reset_parameters()
@@ -115,7 +123,8 @@ class PAMLinear(torch.nn.Module):
                 self.bias.uniform_(-bound, bound)
 
     def forward(self, x: torch.Tensor) -> torch.Tensor:
-        return pam_linear(x, self.weight, self.bias)
+        return pam_linear(x, self.weight, self.bias, self.mantissa_bits)
 
     def extra_repr(self) -> str:
-        return f"in_features={self.in_features}, out_features={self.out_features}, bias={self.bias is not None}"
+        return (f"in_features={self.in_features}, out_features={self.out_features}, bias={self.bias is not None}, "
+                f"mantissa_bits={self.mantissa_bits}")

@@ -94,6 +94,17 @@ struct Paexp2Op {
     }
 };
 
+// Rounding to 23 - drop mantissa bits (the inputs of the narrow matrix
+// product), as an elementwise op.
+struct RoundOp {
+    uint32_t drop;
+    __device__ __forceinline__ uint32_t operator()(uint32_t u) const {
+        const uint32_t low = (1u << drop) - 1u;
+        const uint32_t rounded = (u + (low >> 1) + ((u >> drop) & 1u)) & ~low;
+        return ((u & kInf) == kInf) ? u : rounded;
+    }
+};
+
 template <typename Op>
 __global__ void __launch_bounds__(256) binary_vec4_kernel(const uint4 *__restrict__ a, const uint4 *__restrict__ b,
                                                           uint4 *__restrict__ out, int64_t n4) {
@@ -118,8 +129,7 @@ __global__ void __launch_bounds__(256) binary_scalar_kernel(const uint32_t *__re
 
 template <typename Op>
 __global__ void __launch_bounds__(256) unary_vec4_kernel(const uint4 *__restrict__ a, uint4 *__restrict__ out,
-                                                         int64_t n4) {
-    const Op op;
+                                                         int64_t n4, Op op) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
         const uint4 x = a[i];
@@ -129,8 +139,7 @@ __global__ void __launch_bounds__(256) unary_vec4_kernel(const uint4 *__restrict
 
 template <typename Op>
 __global__ void __launch_bounds__(256) unary_scalar_kernel(const uint32_t *__restrict__ a, uint32_t *__restrict__ out,
-                                                           int64_t n) {
-    const Op op;
+                                                           int64_t n, Op op) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
         out[i] = op(a[i]);
@@ -173,7 +182,7 @@ hipError_t launch_binary(const float *a, const float *b, float *out, int64_t n, 
 }
 
 template <typename Op>
-hipError_t launch_unary(const float *a, float *out, int64_t n, hipStream_t stream) {
+hipError_t launch_unary(const float *a, float *out, int64_t n, hipStream_t stream, Op op = Op()) {
     if (n <= 0)
         return hipSuccess;
     int64_t head = 0;
@@ -182,7 +191,7 @@ hipError_t launch_unary(const float *a, float *out, int64_t n, hipStream_t strea
         if (n4 > 0) {
             const int64_t blocks = std::min<int64_t>((n4 + 255) / 256, kMaxBlocks);
             hipLaunchKernelGGL(unary_vec4_kernel<Op>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                               reinterpret_cast<const uint4 *>(a), reinterpret_cast<uint4 *>(out), n4);
+                               reinterpret_cast<const uint4 *>(a), reinterpret_cast<uint4 *>(out), n4, op);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess)
                 return e;
@@ -194,7 +203,7 @@ hipError_t launch_unary(const float *a, float *out, int64_t n, hipStream_t strea
         const int64_t blocks = std::min<int64_t>((rest + 255) / 256, kMaxBlocks);
         hipLaunchKernelGGL(unary_scalar_kernel<Op>, dim3((unsigned)blocks), dim3(256), 0, stream,
                            reinterpret_cast<const uint32_t *>(a) + head, reinterpret_cast<uint32_t *>(out) + head,
-                           rest);
+                           rest, op);
         return hipGetLastError();
     }
     return hipSuccess;
@@ -212,6 +221,10 @@ hipError_t launch_palog2(const float *a, float *out, int64_t n, hipStream_t stre
 
 hipError_t launch_paexp2(const float *a, float *out, int64_t n, hipStream_t stream) {
     return launch_unary<Paexp2Op>(a, out, n, stream);
+}
+
+hipError_t launch_round_mantissa(const float *a, float *out, int64_t n, int drop, hipStream_t stream) {
+    return launch_unary<RoundOp>(a, out, n, stream, RoundOp{(uint32_t)drop});
 }
 
 }  // namespace pamk

@@ -206,7 +206,7 @@ pam_status_t check_device() {
 
 pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                       int64_t sa, const float *B, int64_t ldb, int64_t sb, float *C, int64_t ldc, int64_t sc,
-                      int64_t batch, const Plan &plan, hipStream_t stream) {
+                      int64_t batch, const Plan &plan, hipStream_t stream, int round_drop = 0) {
     if (m == 0 || n == 0 || batch == 0)
         return PAM_SUCCESS;
     pam_status_t st = check_device();
@@ -237,6 +237,7 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     p.tiles_n = (int32_t)ceil_div(n, plan.tile_n);
     p.vec_a = aligned16(A) && lda % 4 == 0 && (batch == 1 || sa % 4 == 0);
     p.vec_b = aligned16(B) && ldb % 4 == 0 && (batch == 1 || sb % 4 == 0);
+    p.round_drop = round_drop;
 
     const int64_t gz_max = kMaxGridZ;
     float *ws = nullptr;
@@ -394,6 +395,44 @@ pam_status_t pam_gemm_batched(pam_op_t transA, pam_op_t transB, int64_t m, int64
         return PAM_SUCCESS;
     return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch,
                     choose_plan(m, n, k, batch), stream);
+}
+
+pam_status_t pam_gemm_narrow(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k, const float *A,
+                             int64_t lda, int64_t strideA, const float *B, int64_t ldb, int64_t strideB, float *C,
+                             int64_t ldc, int64_t strideC, int64_t batch, int32_t mantissa_bits,
+                             hipStream_t stream) {
+    if (mantissa_bits < 0 || mantissa_bits > 23)
+        return fail(PAM_ERROR_INVALID_VALUE, "mantissa_bits must be in [0, 23]");
+    pam_status_t st = validate(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (m == 0 || n == 0 || batch == 0)
+        return PAM_SUCCESS;
+    return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch,
+                    choose_plan(m, n, k, batch), stream, 23 - mantissa_bits);
+}
+
+pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t mantissa_bits, hipStream_t stream) {
+    if (mantissa_bits < 0 || mantissa_bits > 23)
+        return fail(PAM_ERROR_INVALID_VALUE, "mantissa_bits must be in [0, 23]");
+    if (n < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "n must be >= 0");
+    if (n == 0)
+        return PAM_SUCCESS;
+    if (a == nullptr || out == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "a and out must be non-NULL");
+    pam_status_t st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    hipError_t e;
+    if (mantissa_bits == 23)
+        e = (a == out) ? hipSuccess
+                       : hipMemcpyAsync(out, a, (size_t)n * sizeof(float), hipMemcpyDeviceToDevice, stream);
+    else
+        e = pamk::launch_round_mantissa(a, out, n, 23 - mantissa_bits, stream);
+    if (e != hipSuccess)
+        return fail_hip(e, "pam_round_mantissa launch");
+    return PAM_SUCCESS;
 }
 
 pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_plan_t *plan) {

@@ -25,6 +25,7 @@ struct GemmParams {
     int32_t vec_a;        // float4 global loads of A are aligned
     int32_t vec_b;        // float4 global loads of B are aligned
     int32_t vec_c;        // float4 stores of the output are aligned
+    int32_t round_drop;   // 0, or 23 - m: round every input to m mantissa bits first
 };
 
 hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
@@ -33,6 +34,8 @@ hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n,
 hipError_t launch_pad(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
 hipError_t launch_palog2(const float *a, float *out, int64_t n, hipStream_t stream);
 hipError_t launch_paexp2(const float *a, float *out, int64_t n, hipStream_t stream);
+// Round to 23 - drop mantissa bits, nearest even (drop in [1, 23]).
+hipError_t launch_round_mantissa(const float *a, float *out, int64_t n, int drop, hipStream_t stream);
 
 // (tile_m, tile_n, kgroups) in {(128,128,1), (128,64,1), (64,64,1), (64,64,4)};
 // grid = (tiles_m * tiles_n, splits, batch_in_launch).

@@ -233,6 +233,27 @@ struct TileLoader {
         return make_uint4(e[0], e[1], e[2], e[3]);
     }
 
+    // Round every held element to 23 - drop mantissa bits, nearest even: the
+    // dropped bits plus (half - 1) plus the kept part's lowest bit carry into
+    // the kept part exactly when it must round up; a carry out of the
+    // mantissa moves into the exponent (past the largest one, onto inf).
+    // inf and NaN stay as they are.
+    __device__ __forceinline__ void round_mantissa(int drop) {
+        const uint32_t low = (1u << drop) - 1u;
+        const uint32_t half_m1 = low >> 1;
+#pragma unroll
+        for (int r = 0; r < L; ++r) {
+            uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t u = e[c];
+                const uint32_t rounded = (u + half_m1 + ((u >> drop) & 1u)) & ~low;
+                e[c] = ((u & kExpMask) == kExpMask) ? u : rounded;
+            }
+            v[r] = make_uint4(e[0], e[1], e[2], e[3]);
+        }
+    }
+
     // Scan the held elements.  Returns bit 0 when some element is "tiny" (a
     // normal number with exponent field 1..63, whose products can
     // underflow) and bit 1 when some element needs the SPECIAL path (inf, NaN
@@ -475,6 +496,10 @@ pam_gemm_kernel(GemmParams p) {
 
     const int k_first = grp * KPG;
     for (int c = 0; c < nchunks; ++c) {
+        if (p.round_drop != 0) {
+            la.round_mantissa(p.round_drop);
+            lb.round_mantissa(p.round_drop);
+        }
         const uint32_t f = la.scan() | lb.scan();
         const uint64_t sp = __ballot(f & 2u);
         const uint64_t tn_any = __ballot(f & 1u);

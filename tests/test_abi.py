@@ -79,6 +79,15 @@ def test_empty_products_launch_nothing(lib):
     assert lib.pam_paexp2(None, None, -2, None) == 1
 
 
+def test_narrow_entry_points_reject_bad_mantissa_bits(lib):
+    for bits in (-1, 24, 99):
+        assert lib.pam_gemm_narrow(0, 0, 4, 4, 4, 8, 4, 0, 8, 4, 0, 8, 4, 0, 1, bits, None) == 1
+        assert lib.pam_round_mantissa(8, 8, 4, bits, None) == 1
+    assert lib.pam_round_mantissa(None, None, 0, 7, None) == 0
+    assert lib.pam_gemm_narrow(0, 0, 0, 4, 4, None, 4, 0, 8, 4, 0, None, 4, 0, 1, 7, None) == 0
+    assert lib.pam_gemm_narrow(0, 0, 4, 4, 4, 8, 3, 0, 8, 4, 0, 8, 4, 0, 1, 7, None) == 1   # lda < k
+
+
 def test_elementwise_rejects_null_pointers(lib):
     assert lib.pam_mul(None, 8, 8, 4, None) == 1
     assert lib.pam_pad(8, None, 8, 4, None) == 1

@@ -1,0 +1,126 @@
+"""Narrower-mantissa inputs on the GPU (App. "PAM with Narrower Mantissas",
+reading R11): the elementwise rounding bit-exact against the oracle and held
+to the oracle's pins; the narrow matrix product within the GEMM tolerance of
+the oracle's product of rounded operands."""
+import numpy as np
+import pytest
+
+import narrow_pins
+import pam_workloads as wl
+import paper_2305_17190_amd as pam
+from gpu_util import check_gemm, device, note, oracle_gemm, to_dev
+from oracle import pam_ref
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_round(x, b):
+    x = np.asarray(x, np.float32)
+    return pam.round_mantissa(to_dev(x.reshape(-1)), b).cpu().numpy().reshape(x.shape)
+
+
+@pytest.mark.parametrize("check", narrow_pins.CHECKS, ids=lambda c: c.__name__)
+def test_rounding_pins_on_gpu(check):
+    note(f"round_mantissa pin {check.__name__}")
+    check(gpu_round)
+
+
+@pytest.mark.parametrize("b", [0, 1, 3, 4, 7, 10, 22, 23])
+def test_rounding_bit_exact(b):
+    note(f"round_mantissa bits={b} on 2^20 random patterns + specials")
+    x = np.concatenate([wl.special_bit_patterns(), wl.random_bit_patterns(1 << 20, 600 + b)])
+    got, want = gpu_round(x, b), pam_ref.round_mantissa_ref(x, b)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def narrow_case(ta, tb, m, n, k, bits, seed, batch=1, kind="normal"):
+    g = np.random.default_rng(seed)
+    ar, ac = (k, m) if ta else (m, k)
+    br, bc = (n, k) if tb else (k, n)
+    a = g.standard_normal((batch, ar, ac)).astype(np.float32)
+    b = (g.standard_normal((batch, br, bc)) * 0.05).astype(np.float32)
+    if kind == "edges":
+        # values that round up past FLT_MAX (-> inf), denormals that round to
+        # the min normal, tiny normals whose products underflow
+        flat = a.reshape(-1)
+        idx = g.choice(flat.size, size=max(4, flat.size // 200), replace=False)
+        pick = np.array([0x7F7FFFFF, 0xFF7FF000, 0x007FFFFF, 0x00800001, 0x1F800001], dtype=np.uint32)
+        flat[idx] = pick[g.integers(0, pick.size, size=idx.size)].view(np.float32)
+    note(f"narrow gemm ta={ta} tb={tb} m={m} n={n} k={k} batch={batch} bits={bits} kind={kind}")
+    da, db = to_dev(a), to_dev(b)
+    c = pam.bmm(da, db, ta, tb, mantissa_bits=bits).cpu().numpy()
+    ra, rb = pam_ref.round_mantissa_ref(a, bits), pam_ref.round_mantissa_ref(b, bits)
+    for z in range(batch):
+        cr, sr = pam_ref.pam_gemm_ref(ra[z], rb[z], ta, tb)
+        check_gemm(c[z], cr, sr, k, f"bits={bits} batch {z}")
+
+
+@pytest.mark.parametrize("ta,tb", [(False, False), (False, True), (True, False), (True, True)])
+@pytest.mark.parametrize("bits", [7, 4, 3, 0])
+def test_narrow_gemm_forms(ta, tb, bits):
+    narrow_case(ta, tb, 131, 70, 97, bits, 700 + bits + 2 * ta + tb)
+
+
+def test_narrow_gemm_batched_small_tiles_and_split():
+    narrow_case(False, False, 64, 48, 300, 4, 710, batch=5)            # narrow batched outputs
+    narrow_case(True, False, 96, 80, 2000, 7, 711)                     # long K: split-K
+
+
+def test_narrow_gemm_edge_values():
+    narrow_case(False, True, 70, 66, 120, 7, 712, kind="edges")
+    narrow_case(True, False, 70, 66, 120, 3, 713, kind="edges")
+
+
+def test_full_mantissa_is_the_plain_product():
+    note("narrow gemm bits=23 vs pam_gemm, bitwise")
+    a = wl.random_matrix(300, 200, 714)
+    b = wl.random_matrix(200, 150, 715)
+    da, db = to_dev(a), to_dev(b)
+    c1 = pam.gemm(da, db).cpu().numpy()
+    c2 = pam.bmm(da.unsqueeze(0), db.unsqueeze(0), mantissa_bits=23).cpu().numpy()[0]
+    assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+
+
+def test_narrow_inputs_already_on_grid_match_plain_product():
+    note("operands already on the 4-bit grid: narrow product == plain product, bitwise")
+    a = pam_ref.round_mantissa_ref(wl.random_matrix(257, 129, 716), 4)
+    b = pam_ref.round_mantissa_ref(wl.random_matrix(129, 190, 717), 4)
+    da, db = to_dev(a), to_dev(b)
+    c1 = pam.gemm(da, db).cpu().numpy()
+    c2 = pam.gemm(da, db, mantissa_bits=4).cpu().numpy()
+    assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+
+
+def test_workload5_forward_bfloat16_mantissa_sampled_rows():
+    """The large linear layer's forward with 7-bit mantissas (bfloat16 inputs),
+    sampled rows against the C oracle on rounded operands."""
+    note("w5 fwd bits=7, 8 sampled rows")
+    host = wl.workload_inputs(5, only=["X", "W"])
+    x, w = host["X"], host["W"]
+    y = pam.gemm(to_dev(x), to_dev(w), trans_b=True, mantissa_bits=7)
+    rows = np.random.default_rng(718).choice(x.shape[0], size=8, replace=False)
+    xr = pam_ref.round_mantissa_ref(x[rows], 7)
+    wr = pam_ref.round_mantissa_ref(w, 7)
+    c, s = oracle_gemm(xr, wr, False, True, 8, 4096, 4096, 4096, 4096)
+    check_gemm(y.cpu().numpy()[rows], c[0], s[0], 4096, "w5 fwd bits=7")
+
+
+def test_autograd_with_narrow_mantissas():
+    import torch
+    from paper_2305_17190_amd.autograd import pam_linear
+    note("pam_linear bits=4 forward + backward")
+    dev = device()
+    x = wl.random_matrix(150, 80, 719)
+    w = wl.random_matrix(60, 80, 720, 0.1)
+    g = wl.random_matrix(150, 60, 721, 0.01)
+    xt = torch.from_numpy(x).to(dev).requires_grad_()
+    wt = torch.from_numpy(w).to(dev).requires_grad_()
+    y = pam_linear(xt, wt, None, mantissa_bits=4)
+    y.backward(torch.from_numpy(g).to(dev))
+    r = lambda t: pam_ref.round_mantissa_ref(t, 4)
+    c, s = pam_ref.pam_gemm_ref(r(x), r(w), False, True)
+    check_gemm(y.detach().cpu().numpy(), c, s, 80, "Y bits=4")
+    c, s = pam_ref.pam_gemm_ref(r(g), r(w))
+    check_gemm(xt.grad.cpu().numpy(), c, s, 60, "dX bits=4")
+    c, s = pam_ref.pam_gemm_ref(r(g), r(x), True, False)
+    check_gemm(wt.grad.cpu().numpy(), c, s, 150, "dW bits=4")

@@ -51,6 +51,19 @@ in the HIP library):
       float format's conversion does; inf stays inf and NaN stays NaN.  The
       rounded inputs then go through PAM (R1-R7) with float32 accumulation.
 
+  R15 exact derivative (Table 1: d(A .^ B)/dA = 2^(E_B + 1{M_A + M_B >= 1})):
+      the sign of B is part of it (d(A .^ B)/dA = sgn(B) 2^(E_B + c) for
+      either sign of A, since the magnitude of A .^ B grows with |A| and its
+      sign is S_A + S_B); a zero or denormal A or B gives 0 (A .^ B is
+      identically zero around a zero / denormal B, and flushed to zero
+      around a zero A).  The formula is applied for all normal A, B, also
+      where A .^ B itself under- or overflows.  For a matrix product
+      Y = X .^ W^T the exact derivatives are
+        dX[i,k] = sum_j dY[i,j] d(X[i,k] .^ W[j,k])/dX[i,k]
+        dW[j,k] = sum_i dY[i,j] d(W[j,k] .^ X[i,k])/dW[j,k],
+      the terms exact (a power of two times dY), accumulated in float32.
+      Inf / NaN operands are outside this reading (parity unpinned there).
+
 Three independent renderings of the scalar product are given (bit, field and
 value form); the tests check them against each other and against the facts
 the paper states.
@@ -303,6 +316,42 @@ def pam_gemm_batched_ref(a: np.ndarray, b: np.ndarray, trans_a: bool = False, tr
         cs.append(c)
         ss.append(s)
     return np.stack(cs), np.stack(ss)
+
+
+def pam_exact_grad_factor(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """d(a .^ b)/da in float64 (Table 1, reading R15), elementwise, broadcasting."""
+    a = np.asarray(a, dtype=np.float32)
+    b = np.asarray(b, dtype=np.float32)
+    ua = a.view(np.uint32).astype(np.int64)
+    ub = b.view(np.uint32).astype(np.int64)
+    ea, eb = (ua >> 23) & 0xFF, (ub >> 23) & 0xFF
+    fa, fb = ua & 0x7FFFFF, ub & 0x7FFFFF
+    carry = ((fa + fb) >= (1 << 23)).astype(np.int64)          # 1{M_A + M_B >= 1}
+    sign = np.where(ub >> 31 == 1, -1.0, 1.0)
+    g = sign * np.ldexp(1.0, (eb - 127 + carry).astype(np.int64))
+    return np.where((ea == 0) | (eb == 0), 0.0, g)
+
+
+def pam_exact_grads_ref(dy: np.ndarray, x: np.ndarray, w: np.ndarray):
+    """Exact derivatives of Y = X .^ W^T (Table 1, R15): (dX, S_dX, dW, S_dW)
+    in float64, S = sum of |terms|.  dy [T, N], x [T, K], w [N, K]."""
+    dy = np.asarray(dy, dtype=np.float32).astype(np.float64)
+    t, n = dy.shape
+    k = np.asarray(x).shape[1]
+    dx = np.zeros((t, k))
+    sdx = np.zeros((t, k))
+    dw = np.zeros((n, k))
+    sdw = np.zeros((n, k))
+    for j in range(n):
+        gx = pam_exact_grad_factor(x, w[j:j + 1, :])                  # [T, K]: d(X .^ W[j])/dX
+        term = dy[:, j:j + 1] * gx
+        dx += term
+        sdx += np.abs(term)
+        gw = pam_exact_grad_factor(w[j:j + 1, :], x)                  # [T, K]: d(W[j] .^ X)/dW[j]
+        term = dy[:, j:j + 1] * gw
+        dw[j] = term.sum(axis=0)
+        sdw[j] = np.abs(term).sum(axis=0)
+    return dx, sdx, dw, sdw
 
 
 def gemm_tolerance(s: np.ndarray, k: int) -> np.ndarray:

@@ -32,7 +32,8 @@ ALGO_LANE_OPS_PER_MAC = 2
 # full-rate ops (int32 add, float32 add/mul/fma) = the 157.3 TFLOP/s
 # float32-vector figure counted as one lane op per fma.
 NOMINAL_VALU_LANE_OPS = 256 * 4 * 32 * 2.4e9
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2305_17190_amd", "csrc", "pam_kernels.hip")
+# The GEMM kernel's sources: a committed traffic summary is valid only for these bytes.
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2305_17190_amd", "csrc", f) for f in ("pam_kernels.hip", "pam_tile.h")]
 
 
 def log(msg: str) -> None:
@@ -41,8 +42,11 @@ def log(msg: str) -> None:
 
 
 def kernel_source_digest() -> str:
-    with open(KERNEL_SOURCE, "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def committed_traffic(workload: str, form: str):
@@ -185,10 +189,12 @@ def bench_autograd(args, torch, wl, pam, dev) -> int:
     dy = torch.from_numpy(host["dY"]).to(dev)
     macs = sum(f.macs for f in spec["forms"])
 
+    derivative = "exact" if args.exact_grad else "approximate"
+
     def step():
         x.grad = None
         w.grad = None
-        pam_linear(x, w).backward(dy)
+        pam_linear(x, w, derivative=derivative).backward(dy)
 
     for _ in range(args.warmup):
         step()
@@ -218,7 +224,7 @@ def bench_autograd(args, torch, wl, pam, dev) -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": spec["name"], "layer": "paper_2305_17190_amd.autograd.pam_linear, no bias",
-                   "pam_macs_per_step": macs},
+                   "derivative": derivative, "pam_macs_per_step": macs},
     }
     print(json.dumps(result), flush=True)
     return 0
@@ -240,6 +246,8 @@ def main() -> int:
                     help="round every operand to this many mantissa bits first (narrow products; default 23 = none)")
     ap.add_argument("--autograd", action="store_true",
                     help="time one PAM linear layer forward + backward through autograd (w2, w5)")
+    ap.add_argument("--exact-grad", action="store_true",
+                    help="with --autograd: backward with the exact derivative (Table 1) instead of the approximate one")
     ap.add_argument("--elementwise-op", default="mul", choices=sorted(ELEMENTWISE_OPS),
                     help="the elementwise op --elementwise times (default mul)")
     args = ap.parse_args()

@@ -186,6 +186,27 @@ pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t m
                                 hipStream_t stream);
 
 /*
+ * Exact-derivative PAM products (Table 1): the derivative of A .^ B with
+ * respect to A is sgn(B) 2^(E_B + 1{M_A + M_B >= 1}), a power of two, zero
+ * when A or B is zero or denormal.  This call computes
+ *   C(r, c) = sum_q op(A)(r, q) * d(B(q, c) .^ Mod(r, c)) / dB(q, c)
+ * for 0 <= r < m, 0 <= c < n, q < k, with float32 accumulation of exact terms
+ * (a denormal op(A) element counts as zero).  For Y = X .^ W^T (X: T x K,
+ * W: N x K, dY: T x N):
+ *   dX = (transA = N, A = dY, B = W, Mod = X)   m = T, n = K, k = N
+ *   dW = (transA = T, A = dY, B = X, Mod = W)   m = N, n = K, k = T
+ * op(A) as in pam_gemm; B(q, c) = B[q*ldb + c]; Mod(r, c) = Mod[r*ldm + c];
+ * C(r, c) = C[r*ldc + c] overwritten.  Requirements as pam_gemm (transB = N)
+ * plus ldm >= max(1, n) and Mod non-NULL when m*n > 0.  Inf / NaN operands
+ * give unspecified values.  Long K may use a stream-ordered split-K
+ * workspace as pam_gemm does.
+ */
+pam_status_t pam_gemm_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t k,
+                                 const float *A, int64_t lda, const float *B, int64_t ldb,
+                                 const float *Mod, int64_t ldm, float *C, int64_t ldc,
+                                 hipStream_t stream);
+
+/*
  * Figures of `device` that set the vector-ALU roofline: compute units,
  * SIMDs per compute unit and peak engine clock (kHz) read from the HIP
  * runtime and HSA, wavefront size, and the lanes a SIMD retires per clock

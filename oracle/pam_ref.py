@@ -61,8 +61,9 @@ in the HIP library):
       Y = X .^ W^T the exact derivatives are
         dX[i,k] = sum_j dY[i,j] d(X[i,k] .^ W[j,k])/dX[i,k]
         dW[j,k] = sum_i dY[i,j] d(W[j,k] .^ X[i,k])/dW[j,k],
-      the terms exact (a power of two times dY), accumulated in float32.
-      Inf / NaN operands are outside this reading (parity unpinned there).
+      the terms exact (a power of two times dY; a denormal dY counts as
+      zero, as R3), accumulated in float32.  Inf / NaN operands are outside
+      this reading (parity unpinned there).
 
 Three independent renderings of the scalar product are given (bit, field and
 value form); the tests check them against each other and against the facts
@@ -335,7 +336,8 @@ def pam_exact_grad_factor(a: np.ndarray, b: np.ndarray) -> np.ndarray:
 def pam_exact_grads_ref(dy: np.ndarray, x: np.ndarray, w: np.ndarray):
     """Exact derivatives of Y = X .^ W^T (Table 1, R15): (dX, S_dX, dW, S_dW)
     in float64, S = sum of |terms|.  dy [T, N], x [T, K], w [N, K]."""
-    dy = np.asarray(dy, dtype=np.float32).astype(np.float64)
+    dy = np.asarray(dy, dtype=np.float32)
+    dy = np.where(np.abs(dy) < np.float32(2.0 ** -126), np.float32(0.0), dy).astype(np.float64)   # denormal dY as zero
     t, n = dy.shape
     k = np.asarray(x).shape[1]
     dx = np.zeros((t, k))

@@ -12,6 +12,7 @@ device every call raises.
     round_mantissa(a, bits, out=None)          a rounded to `bits` mantissa bits
     gemm(A, B, trans_a, trans_b, out=None)     C = op(A) .^ op(B)
     bmm(A, B, trans_a, trans_b, out=None)      batched over the leading axis
+    exact_grad(A, B, Mod, trans_a, out=None)   exact-derivative product (Table 1)
 
 Matrix arguments are float32 HIP tensors whose last dimension is contiguous
 (row stride = leading dimension).  op(X) = X^T when trans_x is True.  The
@@ -25,8 +26,8 @@ import ctypes
 import os
 from typing import Optional
 
-__all__ = ["mul", "pad", "palog2", "paexp2", "round_mantissa", "gemm", "bmm", "plan", "device_info",
-           "library_path", "load", "PamError"]
+__all__ = ["mul", "pad", "palog2", "paexp2", "round_mantissa", "gemm", "bmm", "exact_grad", "plan",
+           "device_info", "library_path", "load", "PamError"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libpam.so")
@@ -54,8 +55,8 @@ _lib = None
 
 # Every symbol include/pam.h declares.
 EXPORTS = ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm", "pam_gemm_batched",
-           "pam_gemm_narrow", "pam_gemm_plan", "pam_gemm_batched_with_plan", "pam_device_info", "pam_status_string",
-           "pam_last_error")
+           "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_plan", "pam_gemm_batched_with_plan",
+           "pam_device_info", "pam_status_string", "pam_last_error")
 
 
 def library_path() -> str:
@@ -77,6 +78,7 @@ def load() -> ctypes.CDLL:
     lib.pam_paexp2.argtypes = [vp, vp, i64, vp]
     lib.pam_round_mantissa.argtypes = [vp, vp, i64, i32, vp]
     lib.pam_gemm_narrow.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i32, vp]
+    lib.pam_gemm_exact_grad.argtypes = [i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, i64, vp]
     lib.pam_gemm.argtypes = [i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp]
     lib.pam_gemm_batched.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, vp]
     lib.pam_gemm_batched_with_plan.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64,
@@ -84,8 +86,8 @@ def load() -> ctypes.CDLL:
     lib.pam_gemm_plan.argtypes = [i64, i64, i64, i64, ctypes.POINTER(_Plan)]
     lib.pam_device_info.argtypes = [i32, ctypes.POINTER(_DeviceInfo)]
     for name in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm",
-                 "pam_gemm_batched", "pam_gemm_narrow", "pam_gemm_batched_with_plan", "pam_gemm_plan",
-                 "pam_device_info"):
+                 "pam_gemm_batched", "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_batched_with_plan",
+                 "pam_gemm_plan", "pam_device_info"):
         getattr(lib, name).restype = i32
     lib.pam_status_string.argtypes = [i32]
     lib.pam_status_string.restype = ctypes.c_char_p
@@ -250,6 +252,32 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
     else:
         p = _Plan(*plan) if len(plan) == 4 else _Plan(plan[0], plan[1], plan[2], 1)
         _check(lib.pam_gemm_batched_with_plan(*args, ctypes.byref(p), _stream_handle(A)))
+    return out
+
+
+def exact_grad(A, B, Mod, trans_a: bool = False, out=None):
+    """C(r, c) = sum_q op(A)(r, q) d(B(q, c) .^ Mod(r, c)) / dB(q, c) (Table 1's
+    exact derivative).  For Y = X .^ W^T: dX = exact_grad(dY, W, X) and
+    dW = exact_grad(dY, X, W, trans_a=True)."""
+    torch = _torch()
+    _require(A, "A", 2)
+    _require(B, "B", 2)
+    _require(Mod, "Mod", 2)
+    m, k = (A.shape[1], A.shape[0]) if trans_a else (A.shape[0], A.shape[1])
+    if B.shape[0] != k:
+        raise ValueError(f"inner dimensions differ: op(A) is {m}x{k}, B is {tuple(B.shape)}")
+    n = B.shape[1]
+    if tuple(Mod.shape) != (m, n):
+        raise ValueError(f"Mod must be {m}x{n}")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=A.device)
+    else:
+        _require(out, "out", 2)
+        if tuple(out.shape) != (m, n):
+            raise ValueError(f"out must be {m}x{n}")
+    _check(load().pam_gemm_exact_grad(PAM_OP_T if trans_a else PAM_OP_N, m, n, k, A.data_ptr(), _ld(A),
+                                      B.data_ptr(), _ld(B), Mod.data_ptr(), _ld(Mod), out.data_ptr(), _ld(out),
+                                      _stream_handle(A)))
     return out
 
 

@@ -10,7 +10,10 @@ matrix multiply's gradients are ordinary products.
     C = A .^ B (batched)   dA = dC .^ B^T     dB = A^T .^ dC
 
 Every product runs in the library's HIP kernels (``pam.gemm`` / ``pam.bmm``);
-the bias gradient is an ordinary sum (no multiplication).  With
+the bias gradient is an ordinary sum (no multiplication).  ``pam_linear``
+and ``PAMLinear`` also offer Table 1's exact derivative
+(``derivative="exact"``): dX[i,k] = sum_j dY[i,j] d(X[i,k] .^ W[j,k])/dX[i,k]
+and dW likewise, through ``pam.exact_grad``.  With
 ``mantissa_bits`` < 23 every product, forward and backward, first rounds its
 two operands to that many mantissa bits (App. "PAM with Narrower
 Mantissas"); the tensors themselves are not modified.  Inputs must be float32
@@ -23,6 +26,7 @@ import math
 import torch
 
 from . import bmm as _bmm
+from . import exact_grad as _exact_grad
 from . import gemm as _gemm
 
 __all__ = ["pam_linear", "pam_matmul", "PAMLinear"]
@@ -37,12 +41,13 @@ def _last_contiguous(t: torch.Tensor) -> torch.Tensor:
 
 class _PAMLinearFn(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, x2d, weight, bias, bits):
+    def forward(ctx, x2d, weight, bias, bits, exact):
         x2d = _last_contiguous(x2d)
         weight = _last_contiguous(weight)
         ctx.save_for_backward(x2d, weight)
         ctx.has_bias = bias is not None
         ctx.bits = bits
+        ctx.exact = exact
         y = _gemm(x2d, weight, trans_b=True, mantissa_bits=bits)   # Y = X .^ W^T
         if bias is not None:
             y += bias
@@ -53,22 +58,35 @@ class _PAMLinearFn(torch.autograd.Function):
         x2d, weight = ctx.saved_tensors
         dy = _last_contiguous(dy)
         dx = dw = db = None
-        if ctx.needs_input_grad[0]:
-            dx = _gemm(dy, weight, mantissa_bits=ctx.bits)                  # dX = dY .^ W
-        if ctx.needs_input_grad[1]:
-            dw = _gemm(dy, x2d, trans_a=True, mantissa_bits=ctx.bits)       # dW = dY^T .^ X
+        if ctx.exact:
+            if ctx.needs_input_grad[0]:
+                dx = _exact_grad(dy, weight, x2d)                           # sum_j dY d(X .^ W)/dX
+            if ctx.needs_input_grad[1]:
+                dw = _exact_grad(dy, x2d, weight, trans_a=True)             # sum_i dY d(W .^ X)/dW
+        else:
+            if ctx.needs_input_grad[0]:
+                dx = _gemm(dy, weight, mantissa_bits=ctx.bits)              # dX = dY .^ W
+            if ctx.needs_input_grad[1]:
+                dw = _gemm(dy, x2d, trans_a=True, mantissa_bits=ctx.bits)   # dW = dY^T .^ X
         if ctx.has_bias and ctx.needs_input_grad[2]:
             db = dy.sum(dim=0)
-        return dx, dw, db, None
+        return dx, dw, db, None, None
 
 
 def pam_linear(x: torch.Tensor, weight: torch.Tensor, bias: torch.Tensor = None,
-               mantissa_bits: int = 23) -> torch.Tensor:
-    """``x .^ weight^T + bias`` over the last dimension of x (any leading dims)."""
+               mantissa_bits: int = 23, derivative: str = "approximate") -> torch.Tensor:
+    """``x .^ weight^T + bias`` over the last dimension of x (any leading dims).
+
+    ``derivative``: "approximate" (Table 1's approximate derivative, PAM
+    products) or "exact" (Table 1's exact derivative)."""
     if x.dim() < 1:
         raise ValueError("x must have at least one dimension")
+    if derivative not in ("approximate", "exact"):
+        raise ValueError('derivative must be "approximate" or "exact"')
+    if derivative == "exact" and mantissa_bits != 23:
+        raise ValueError("the exact derivative takes full float32 mantissas")
     lead = x.shape[:-1]
-    y = _PAMLinearFn.apply(x.reshape(-1, x.shape[-1]), weight, bias, int(mantissa_bits))
+    y = _PAMLinearFn.apply(x.reshape(-1, x.shape[-1]), weight, bias, int(mantissa_bits), derivative == "exact")
     return y.reshape(*lead, weight.shape[0])
 
 
@@ -106,11 +124,12 @@ class PAMLinear(torch.nn.Module):
     """A linear layer whose products are PAM (forward and approximate-derivative backward)."""
 
     def __init__(self, in_features: int, out_features: int, bias: bool = True, device=None,
-                 mantissa_bits: int = 23):
+                 mantissa_bits: int = 23, derivative: str = "approximate"):
         super().__init__()
         self.in_features = in_features
         self.out_features = out_features
         self.mantissa_bits = mantissa_bits
+        self.derivative = derivative
         self.weight = torch.nn.Parameter(torch.empty(out_features, in_features, device=device))
         self.bias = torch.nn.Parameter(torch.empty(out_features, device=device)) if bias else None
         self.reset_parameters()
@@ -123,8 +142,8 @@ class PAMLinear(torch.nn.Module):
                 self.bias.uniform_(-bound, bound)
 
     def forward(self, x: torch.Tensor) -> torch.Tensor:
-        return pam_linear(x, self.weight, self.bias, self.mantissa_bits)
+        return pam_linear(x, self.weight, self.bias, self.mantissa_bits, self.derivative)
 
     def extra_repr(self) -> str:
         return (f"in_features={self.in_features}, out_features={self.out_features}, bias={self.bias is not None}, "
-                f"mantissa_bits={self.mantissa_bits}")
+                f"mantissa_bits={self.mantissa_bits}, derivative={self.derivative}")

@@ -435,6 +435,74 @@ pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t m
     return PAM_SUCCESS;
 }
 
+pam_status_t pam_gemm_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                                 const float *B, int64_t ldb, const float *Mod, int64_t ldm, float *C, int64_t ldc,
+                                 hipStream_t stream) {
+    pam_status_t st = validate(transA, PAM_OP_N, m, n, k, A, lda, 0, B, ldb, 0, C, ldc, 0, 1);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (ldm < std::max<int64_t>(1, n))
+        return fail(PAM_ERROR_INVALID_VALUE, "ldm must be >= max(1, n)");
+    if (m == 0 || n == 0)
+        return PAM_SUCCESS;
+    if (Mod == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "Mod is NULL");
+    st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    if (k == 0) {
+        hipError_t e = pamk::launch_fill_zero(C, (int32_t)m, (int32_t)n, ldc, 0, 1, stream);
+        return e == hipSuccess ? PAM_SUCCESS : fail_hip(e, "fill kernel launch");
+    }
+    // 128 x 128 tiles, two workgroups per compute unit; split K while the
+    // tiles would not fill two rounds and each slice keeps >= 4 chunks.
+    const int64_t tiles = ceil_div(m, 128) * ceil_div(n, 128);
+    int64_t splits = 1;
+    while (tiles * splits < 4 * kComputeUnits && splits < kMaxSplits && k / (splits * 2) >= 4 * pamk::kChunkK)
+        splits *= 2;
+    pamk::GemmParams p{};
+    p.A = A;
+    p.B = B;
+    p.Mod = Mod;
+    p.lda = lda;
+    p.ldb = ldb;
+    p.ldm = ldm;
+    p.ldc = ldc;
+    p.m = (int32_t)m;
+    p.n = (int32_t)n;
+    p.k = (int32_t)k;
+    p.k_per_split = (int32_t)(ceil_div(ceil_div(k, splits), pamk::kChunkK) * pamk::kChunkK);
+    p.splits = (int32_t)ceil_div(k, p.k_per_split);
+    p.tiles_n = (int32_t)ceil_div(n, 128);
+    p.vec_a = aligned16(A) && lda % 4 == 0;
+    p.vec_b = aligned16(B) && ldb % 4 == 0;
+    float *ws = nullptr;
+    if (p.splits > 1) {
+        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), (size_t)p.splits * m * n * sizeof(float), stream);
+        if (e != hipSuccess || ws == nullptr) {
+            g_last_error = std::string("hipMallocAsync of the split-K workspace: ") + hipGetErrorString(e);
+            return PAM_ERROR_ALLOC;
+        }
+    }
+    p.C = C;
+    p.W = ws;
+    pam_status_t result = PAM_SUCCESS;
+    hipError_t e = pamk::launch_pam_exact_grad(transA == PAM_OP_T, p, stream);
+    if (e != hipSuccess)
+        result = fail_hip(e, "exact-derivative kernel launch");
+    else if (ws) {
+        e = pamk::launch_splitk_reduce(ws, C, (int32_t)m, (int32_t)n, ldc, 0, p.splits, 1, stream);
+        if (e != hipSuccess)
+            result = fail_hip(e, "split-K reduce launch");
+    }
+    if (ws) {
+        e = hipFreeAsync(ws, stream);
+        if (e != hipSuccess && result == PAM_SUCCESS)
+            result = fail_hip(e, "hipFreeAsync of the split-K workspace");
+    }
+    return result;
+}
+
 pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_plan_t *plan) {
     if (plan == nullptr)
         return fail(PAM_ERROR_INVALID_VALUE, "plan is NULL");

@@ -26,6 +26,10 @@ struct GemmParams {
     int32_t vec_b;        // float4 global loads of B are aligned
     int32_t vec_c;        // float4 stores of the output are aligned
     int32_t round_drop;   // 0, or 23 - m: round every input to m mantissa bits first
+    // Exact-derivative products only: the output-shaped operand whose
+    // mantissas set each term's carry (row-major, leading dimension ldm).
+    const float *Mod;
+    int64_t ldm;
 };
 
 hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream);
@@ -41,6 +45,10 @@ hipError_t launch_round_mantissa(const float *a, float *out, int64_t n, int drop
 // grid = (tiles_m * tiles_n, splits, batch_in_launch).
 hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b,
                            const GemmParams &p, int64_t batch, hipStream_t stream);
+
+// Exact-derivative product (pam_exact_grad.hip): C(r, c) = sum_q op(A)(r, q)
+// d(B(q, c) .^ Mod(r, c)) / dB(q, c); 128 x 128 tiles, grid (tiles, splits).
+hipError_t launch_pam_exact_grad(bool trans_a, const GemmParams &p, hipStream_t stream);
 
 // C[b][i][j] = sum_s W[b][s][i][j], s in increasing order.
 hipError_t launch_splitk_reduce(const float *W, float *C, int32_t m, int32_t n, int64_t ldc,

@@ -46,20 +46,9 @@
 #include <algorithm>
 
 #include "pam_internal.h"
+#include "pam_tile.h"
 
 namespace pamk {
-
-constexpr uint32_t kSign = 0x80000000u;
-constexpr uint32_t kMag = 0x7FFFFFFFu;
-constexpr uint32_t kBias = 0x3F800000u;     // 127 << 23
-constexpr uint32_t kMinNormal = 0x00800000u;
-constexpr uint32_t kFltMax = 0x7F7FFFFFu;
-constexpr uint32_t kInf = 0x7F800000u;
-constexpr uint32_t kQNaN = 0x7FC00000u;
-constexpr uint32_t kExpMask = 0x7F800000u;
-
-constexpr uint32_t kSignExp = 0xFF800000u;
-constexpr uint32_t kMant = 0x007FFFFFu;
 
 enum : int { kScaled = 0, kSpecial = 1 };
 
@@ -147,194 +136,6 @@ hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n,
 // Tiled PAM matrix product
 // ---------------------------------------------------------------------------
 
-// An operand tile of D (rows of op(A), or columns of op(B)) x kChunkK, staged
-// through registers.  KCONTIG: element (o, kk) of chunk c sits at
-// base + (o0 + o) * ld + k0 + kk (A with op N, B with op T); otherwise at
-// base + (k0 + kk) * ld + o0 + o (A with op T, B with op N).  Each thread
-// holds L groups of four elements consecutive in memory.  The byte offset of
-// each group from the chunk's base is fixed for the whole K loop, so the base
-// (uniform, in scalar registers) is the only address that moves.
-template <int D, int NT, int BK, bool KCONTIG>
-struct TileLoader {
-    static constexpr int L = D * BK / 4 / NT;
-    static_assert(L >= 1 && D * BK / 4 == L * NT, "tile does not divide over the threads");
-    uint4 v[L];
-    uint32_t boff[L];   // byte offset of the group from the chunk base
-    uint32_t edge;      // bit r: group r straddles the last valid row (OCONTIG) -- per-element path
-
-    // Group r of thread tid: KCONTIG -> (row o, k offset kq); else (k row kk, first o oq).
-    static __device__ __forceinline__ int grp_o(int tid, int r) {
-        const int f = tid + NT * r;
-        return KCONTIG ? f / (BK / 4) : (f % (D / 4)) * 4;
-    }
-    static __device__ __forceinline__ int grp_k(int tid, int r) {
-        const int f = tid + NT * r;
-        return KCONTIG ? (f % (BK / 4)) * 4 : f / (D / 4);
-    }
-
-    // Rows past o_lim are clamped to the last valid row (their outputs are
-    // discarded); the clamp is fixed for the whole K loop.
-    __device__ __forceinline__ void init(int64_t ld, int o0, int o_lim, int tid) {
-        edge = 0;
-#pragma unroll
-        for (int r = 0; r < L; ++r) {
-            const int o = grp_o(tid, r);
-            const int kk = grp_k(tid, r);
-            if (KCONTIG) {
-                const int row = min(o0 + o, o_lim - 1) - o0;
-                boff[r] = (uint32_t)((row * ld + kk) * 4);
-            } else {
-                boff[r] = (uint32_t)((kk * ld + o) * 4);
-                if (o0 + o + 3 >= o_lim)
-                    edge |= 1u << r;
-            }
-        }
-    }
-
-    // Load chunk elements [k0, k0 + BK) of the panel whose chunk base is
-    // `base`.  Elements at k >= k_lim are zero (they must add nothing).
-    __device__ __forceinline__ void load(const float *__restrict__ base, int o0, int o_lim, int k0, int k_lim,
-                                         bool vec, int tid) {
-        const char *cb = reinterpret_cast<const char *>(base);
-        if (vec && k0 + BK <= k_lim) {
-            // Interior chunk, aligned operand: one 16-byte load per group.
-#pragma unroll
-            for (int r = 0; r < L; ++r) {
-                if (KCONTIG || !((edge >> r) & 1u))
-                    v[r] = *reinterpret_cast<const uint4 *>(cb + boff[r]);
-                else
-                    v[r] = load_elements(cb, r, o0, o_lim, k0, k_lim, tid);
-            }
-        } else {
-#pragma unroll
-            for (int r = 0; r < L; ++r)
-                v[r] = load_elements(cb, r, o0, o_lim, k0, k_lim, tid);
-        }
-    }
-
-    // Group r element by element, with the K tail and (OCONTIG) the last
-    // valid row applied.
-    __device__ __forceinline__ uint4 load_elements(const char *cb, int r, int o0, int o_lim, int k0, int k_lim,
-                                                   int tid) const {
-        const float *src = reinterpret_cast<const float *>(cb + boff[r]);
-        const int kk = grp_k(tid, r);
-        uint32_t e[4];
-        if (KCONTIG) {
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                e[c] = (k0 + kk + c < k_lim) ? __float_as_uint(src[c]) : 0u;
-        } else {
-            const int o = grp_o(tid, r);
-            const float *row = src - o;
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                e[c] = (k0 + kk < k_lim) ? __float_as_uint(row[min(o0 + o + c, o_lim - 1) - o0]) : 0u;
-        }
-        return make_uint4(e[0], e[1], e[2], e[3]);
-    }
-
-    // Round every held element to 23 - drop mantissa bits, nearest even: the
-    // dropped bits plus (half - 1) plus the kept part's lowest bit carry into
-    // the kept part exactly when it must round up; a carry out of the
-    // mantissa moves into the exponent (past the largest one, onto inf).
-    // inf and NaN stay as they are.
-    __device__ __forceinline__ void round_mantissa(int drop) {
-        const uint32_t low = (1u << drop) - 1u;
-        const uint32_t half_m1 = low >> 1;
-#pragma unroll
-        for (int r = 0; r < L; ++r) {
-            uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t u = e[c];
-                const uint32_t rounded = (u + half_m1 + ((u >> drop) & 1u)) & ~low;
-                e[c] = ((u & kExpMask) == kExpMask) ? u : rounded;
-            }
-            v[r] = make_uint4(e[0], e[1], e[2], e[3]);
-        }
-    }
-
-    // Scan the held elements.  Returns bit 0 when some element is "tiny" (a
-    // normal number with exponent field 1..63, whose products can
-    // underflow) and bit 1 when some element needs the SPECIAL path (inf, NaN
-    // or |x| >= 2^64).  Zeros and denormals are neither.
-    __device__ __forceinline__ uint32_t scan() const {
-        uint32_t hi = 0, lo = 0xFFFFFFFFu;
-#pragma unroll
-        for (int r = 0; r < L; ++r) {
-            const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t ex = e[c] & kExpMask;
-                hi = max(hi, ex);
-                lo = min(lo, ex - kMinNormal);   // a zero field wraps to the top
-            }
-        }
-        return (lo < (63u << 23) ? 1u : 0u) | (hi >= (191u << 23) ? 2u : 0u);
-    }
-
-    // "Tiny": a normal number with exponent field 1..63.
-    __device__ __forceinline__ static bool tiny(uint32_t u) {
-        return (u & kExpMask) - kMinNormal < (63u << 23);
-    }
-
-    // Write the chunk into LDS buffer s, k-major: s[plane][kk][o].  A: plane 0
-    // aM (1 + M), plane 1 m (+-2^E or +-0); B: plane 0 b' (b - bias, zero and
-    // denormal b as a signed zero first).  When `has_tiny`, a tiny element at
-    // chunk step k sets bit k % 16 of mask[(k / 16) * (b_slot + 1) + w], w
-    // being the row wave that reads it (A) or b_slot (B).
-    template <int LDS_LD, typename RowWave>
-    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], bool is_b, int tid, bool has_tiny,
-                                          uint32_t *mask, int b_slot, RowWave row_wave) const {
-#pragma unroll
-        for (int r = 0; r < L; ++r) {
-            const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
-            uint32_t p0[4], p1[4];
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t u = e[c];
-                if (is_b) {
-                    // Multiplying by 1.0 flushes a denormal to the signed
-                    // zero (denormals are flushed); everything else passes
-                    // unchanged (a NaN stays a NaN).
-                    uint32_t f;
-                    asm("v_mul_f32 %0, 1.0, %1" : "=v"(f) : "v"(u));
-                    p0[c] = f - kBias;
-                    p1[c] = 0u;
-                } else {
-                    p0[c] = (u & kMant) | kBias;
-                    p1[c] = u & kSignExp;
-                }
-            }
-            const int o = grp_o(tid, r);
-            const int kk = grp_k(tid, r);
-            if (KCONTIG) {
-#pragma unroll
-                for (int c = 0; c < 4; ++c)
-                    s[0][kk + c][o] = p0[c];
-                if (!is_b) {
-#pragma unroll
-                    for (int c = 0; c < 4; ++c)
-                        s[1][kk + c][o] = p1[c];
-                }
-            } else {
-                *reinterpret_cast<uint4 *>(&s[0][kk][o]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
-                if (!is_b)
-                    *reinterpret_cast<uint4 *>(&s[1][kk][o]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
-            }
-            if (has_tiny) {
-#pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    if (tiny(e[c])) {
-                        const int k = KCONTIG ? kk + c : kk;
-                        atomicOr(&mask[(k / 16) * (b_slot + 1) + (is_b ? b_slot : row_wave(KCONTIG ? o : o + c))],
-                                 1u << (k % 16));
-                    }
-                }
-            }
-        }
-    }
-};
 
 // One micro-tile row, S2: acc[j] = fma(aM + b'[j], m, acc[j]) for j < 8.
 // The eight integer adds are issued before the eight fmas: a SIMD pairs the
@@ -401,14 +202,6 @@ __device__ __forceinline__ void s3_row(float (&acc)[8], uint32_t am, uint32_t m,
           "v"(bb[7]));
 }
 
-template <int BK, int LD>
-__device__ __forceinline__ void lds_frag(const uint32_t (*s)[BK][LD], int plane, int kk, int i0, int half,
-                                         uint32_t out[8]) {
-    const uint4 lo = *reinterpret_cast<const uint4 *>(&s[plane][kk][i0]);
-    const uint4 hi = *reinterpret_cast<const uint4 *>(&s[plane][kk][half + i0]);
-    out[0] = lo.x; out[1] = lo.y; out[2] = lo.z; out[3] = lo.w;
-    out[4] = hi.x; out[5] = hi.y; out[6] = hi.z; out[7] = hi.w;
-}
 
 // Waves each SIMD holds for a tile shape (the register budget per wave is
 // 512 / waves): three for the 128 x 128 tile, whose loop fits 168 registers;

@@ -154,3 +154,12 @@ def test_autograd_wrappers_refuse_cpu_tensors():
         lin(torch.ones(2, 4))
     with pytest.raises(pam.PamError):
         pam_matmul(torch.ones(2, 2), torch.ones(2, 2))
+
+
+def test_exact_grad_rejects_bad_arguments(lib):
+    # transA N: lda >= k, ldb >= n, ldm >= n, ldc >= n
+    assert lib.pam_gemm_exact_grad(0, 4, 4, 4, 8, 4, 8, 4, 8, 3, 8, 4, None) == 1      # ldm < n
+    assert lib.pam_gemm_exact_grad(0, 4, 4, 4, 8, 3, 8, 4, 8, 4, 8, 4, None) == 1      # lda < k
+    assert lib.pam_gemm_exact_grad(0, 4, 4, 4, 8, 4, 8, 4, None, 4, 8, 4, None) == 1   # Mod NULL
+    assert lib.pam_gemm_exact_grad(2, 4, 4, 4, 8, 4, 8, 4, 8, 4, 8, 4, None) == 1      # bad transA
+    assert lib.pam_gemm_exact_grad(0, 0, 4, 4, None, 4, 8, 4, None, 4, None, 4, None) == 0   # m == 0

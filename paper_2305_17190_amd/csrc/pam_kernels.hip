@@ -14,13 +14,21 @@
 // fma issue at twice the rate of other vector ops (max, add3, saturating
 // add), so the per-MAC work is built from those four only.
 //
-// SCALED encoding (written to LDS once per chunk):
+// Encodings written to LDS once per chunk:
 //   A element a = (-1)^s 2^E (1 + M):  aM = encoding of 1 + M (exponent
-//       field 127, a's mantissa) and m = a with its mantissa cleared, i.e.
-//       the float +-2^E, or +-0 when a is zero/denormal.
+//       field 127, a's mantissa), m = a with its mantissa cleared, i.e.
+//       the float +-2^E, or +-0 when a is zero/denormal, and a itself.
 //   B element b:  b' = encoding of b minus 0x3F800000 (zero and denormal b
 //       are encoded as a signed zero first).
-//   Then t = aM + b' (one int add) is the encoding of PAM(1 + M, b): adding
+//
+//   S1 (per MAC: v_add_u32, v_add_f32): acc += a + b'.  When both exponent
+//      fields are in [64, 190] the int32 sum is PAM(a, b)'s encoding itself
+//      (Sec. 2.2's addition; the magnitude sum cannot leave the normal range
+//      and the carry out of the sign bits leaves their exclusive or), so one
+//      float add accumulates it: no multiply at all.
+//
+//   SCALED form, for the other finite operands: t = aM + b' (one int add) is
+//   the encoding of PAM(1 + M, b): adding
 //   1 + M's mantissa to b's encoding is Sec. 2.2's sum with E = 0 on the A
 //   side.  PAM is exact under power-of-two scaling (Fig. 2: the pattern
 //   repeats per octave), so t * m = PAM(a, b) whenever the result is a normal
@@ -33,8 +41,10 @@
 //   S3 (per MAC: v_add_u32, v_mul_f32, v_add_f32): p = t * m is rounded on
 //      its own, so an underflowing product flushes to the signed zero PAM
 //      defines; exact for all finite operands with |x| < 2^64.
-//   Each wave picks S2 or S3 per k step from a bit mask of the operands it
-//   will read at that k ("tiny": nonzero with exponent field 1..63).
+//   Each wave picks S1, S2 or S3 per k step from bit masks of the operands
+//   it will read at that k: S1 unless one has exponent field below 64, S3 if
+//   one of those is a normal number ("tiny", field 1..63), S2 otherwise
+//   (zeros and denormals only).
 //
 // SPECIAL: a chunk holding inf, NaN or |x| >= 2^64 is written raw and
 // evaluated with the complete per-MAC definition (never taken on finite data
@@ -137,6 +147,36 @@ hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n,
 // ---------------------------------------------------------------------------
 
 
+// One micro-tile row, S1: acc[j] += a + b'[j] for j < 8.  When a and every
+// b[j] have exponent fields in [64, 190], the int32 sum of a's encoding and
+// b' = b - bias is the encoding of PAM(a, b) itself: the magnitude sum stays
+// within [2^23, 255 * 2^23), so no range check applies, and the carry out of
+// the sign bits leaves their exclusive or.  No multiply.
+__device__ __forceinline__ void s1_row(float (&acc)[8], uint32_t a, const uint32_t (&bb)[8]) {
+    uint32_t t0, t1, t2, t3, t4, t5, t6, t7;
+    asm("v_add_u32 %0, %16, %17\n\t"
+        "v_add_u32 %1, %16, %18\n\t"
+        "v_add_u32 %2, %16, %19\n\t"
+        "v_add_u32 %3, %16, %20\n\t"
+        "v_add_u32 %4, %16, %21\n\t"
+        "v_add_u32 %5, %16, %22\n\t"
+        "v_add_u32 %6, %16, %23\n\t"
+        "v_add_u32 %7, %16, %24\n\t"
+        "v_add_f32 %8, %8, %0\n\t"
+        "v_add_f32 %9, %9, %1\n\t"
+        "v_add_f32 %10, %10, %2\n\t"
+        "v_add_f32 %11, %11, %3\n\t"
+        "v_add_f32 %12, %12, %4\n\t"
+        "v_add_f32 %13, %13, %5\n\t"
+        "v_add_f32 %14, %14, %6\n\t"
+        "v_add_f32 %15, %15, %7"
+        : "=&v"(t0), "=&v"(t1), "=&v"(t2), "=&v"(t3), "=&v"(t4), "=&v"(t5), "=&v"(t6), "=&v"(t7),
+          "+v"(acc[0]), "+v"(acc[1]), "+v"(acc[2]), "+v"(acc[3]), "+v"(acc[4]), "+v"(acc[5]), "+v"(acc[6]),
+          "+v"(acc[7])
+        : "v"(a), "v"(bb[0]), "v"(bb[1]), "v"(bb[2]), "v"(bb[3]), "v"(bb[4]), "v"(bb[5]), "v"(bb[6]),
+          "v"(bb[7]));
+}
+
 // One micro-tile row, S2: acc[j] = fma(aM + b'[j], m, acc[j]) for j < 8.
 // The eight integer adds are issued before the eight fmas: a SIMD pairs the
 // full-rate ops of two waves only when neither wave stalls on the result of
@@ -233,13 +273,13 @@ pam_gemm_kernel(GemmParams p) {
 
     // The chunk in LDS, and for KW > 1 the partial tiles, which reuse the
     // same bytes after the K loop.
-    constexpr int kTileWords = 2 * BK * LDA + BK * LDB;
+    constexpr int kTileWords = 3 * BK * LDA + BK * LDB;
     constexpr int kRedWords = KW > 1 ? KW * BM * LDR : 0;
     __shared__ __attribute__((aligned(16))) uint32_t smem[kTileWords > kRedWords ? kTileWords : kRedWords];
     __shared__ uint32_t sVote[NW];                 // chunk needs the SPECIAL path
-    __shared__ uint32_t sMask[2][KW * (NRW + 1)];  // [chunk parity] tiny bits per (group, row wave / B)
-    uint32_t (*sA)[BK][LDA] = reinterpret_cast<uint32_t (*)[BK][LDA]>(smem);             // plane 0 aM, 1 m
-    uint32_t (*sB)[BK][LDB] = reinterpret_cast<uint32_t (*)[BK][LDB]>(smem + 2 * BK * LDA);  // b'
+    __shared__ uint32_t sMask[2][KW * (NRW + 1)];  // [chunk parity] low / tiny bits per (group, row wave / B)
+    uint32_t (*sA)[BK][LDA] = reinterpret_cast<uint32_t (*)[BK][LDA]>(smem);             // plane 0 aM, 1 m, 2 a
+    uint32_t (*sB)[BK][LDB] = reinterpret_cast<uint32_t (*)[BK][LDB]>(smem + 3 * BK * LDA);  // b'
 
     const int tid = threadIdx.x;
     const int grp = tid / NTG;
@@ -295,11 +335,11 @@ pam_gemm_kernel(GemmParams p) {
         }
         const uint32_t f = la.scan() | lb.scan();
         const uint64_t sp = __ballot(f & 2u);
-        const uint64_t tn_any = __ballot(f & 1u);
+        const uint64_t low_any = __ballot(f & 1u);
         uint32_t *mask = sMask[c & 1];
         __syncthreads();   // every wave is done reading the previous chunk (and zeroing this mask)
-        la.template store<LDA>(sA, false, tid, tn_any != 0, mask, NRW, row_wave);
-        lb.template store<LDB>(sB, true, tid, tn_any != 0, mask, NRW, row_wave);
+        la.template store<LDA>(sA, false, tid, low_any != 0, mask, NRW, row_wave);
+        lb.template store<LDB>(sB, true, tid, low_any != 0, mask, NRW, row_wave);
         if ((tid & 63) == 0)
             sVote[wave] = sp ? 1u : 0u;
         __syncthreads();
@@ -309,8 +349,10 @@ pam_gemm_kernel(GemmParams p) {
         for (int w = 0; w < NW; ++w)
             v |= sVote[w];
         const bool special = v != 0u;
-        const uint32_t slow =
-            __builtin_amdgcn_readfirstlane(mask[grp * (NRW + 1) + rwave] | mask[grp * (NRW + 1) + NRW]) & 0xFFFFu;
+        // Bits 0..15: the wave's k steps with an operand of exponent field
+        // below 64; bits 16..31: those among them with a tiny normal one.
+        const uint32_t low =
+            __builtin_amdgcn_readfirstlane(mask[grp * (NRW + 1) + rwave] | mask[grp * (NRW + 1) + NRW]);
         if (tid < KW * (NRW + 1))
             sMask[(c + 1) & 1][tid] = 0u;   // next chunk's masks; last read one chunk ago
 
@@ -322,14 +364,26 @@ pam_gemm_kernel(GemmParams p) {
 
         const uint32_t (*cA)[BK][LDA] = sA;
         const uint32_t (*cB)[BK][LDB] = sB;
-        // The wave's k steps of this chunk as three bit sets, taken by three
-        // loops in sequence (accumulation order is free): S2 steps, S3 steps,
+        // The wave's k steps of this chunk as four bit sets, taken by four
+        // loops in sequence (accumulation order is free): S1 steps (every
+        // operand's exponent field in [64, 190]), S2 steps (zeros or
+        // denormals among them, no tiny normals), S3 steps (tiny normals),
         // and for a SPECIAL chunk every step with the complete definition.
         // Loops in sequence, rather than alternative paths, keep the
         // accumulator tile in one set of registers.
-        const uint32_t s2_bits = special ? 0u : (~slow & 0xFFFFu);
-        const uint32_t s3_bits = special ? 0u : slow;
+        const uint32_t s1_bits = special ? 0u : (~low & 0xFFFFu);
+        const uint32_t s2_bits = special ? 0u : (low & ~(low >> 16) & 0xFFFFu);
+        const uint32_t s3_bits = special ? 0u : (low >> 16);
         const uint32_t sp_bits = special ? 0xFFFFu : 0u;
+        for (uint32_t todo = s1_bits; todo != 0u; todo &= todo - 1u) {
+            const int kk = k_first + __builtin_ctz(todo);
+            uint32_t aa[8], bb[8];
+            lds_frag<BK, LDA>(cA, 2, kk, ty * 4, HM, aa);
+            lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                s1_row(acc[i], aa[i], bb);
+        }
         for (uint32_t todo = s2_bits; todo != 0u; todo &= todo - 1u) {
             const int kk = k_first + __builtin_ctz(todo);
             uint32_t am[8], mm[8], bb[8];
@@ -350,22 +404,19 @@ pam_gemm_kernel(GemmParams p) {
             for (int i = 0; i < 8; ++i)
                 s3_row(acc[i], am[i], mm[i], bb);
         }
-        // SPECIAL: rebuild each operand's encoding (A: sign and exponent from
-        // m, mantissa from aM; B: b' + bias, denormals already zero) and
-        // apply the complete definition per MAC.
+        // SPECIAL: the complete definition per MAC on the operands' own
+        // encodings (A: plane 2; B: b' + bias, denormals already zero).
 #pragma unroll 1
         for (uint32_t todo = sp_bits; todo != 0u; todo &= todo - 1u) {
             const int kk = k_first + __builtin_ctz(todo);
-            uint32_t am[8], mm[8], bb[8];
-            lds_frag<BK, LDA>(cA, 0, kk, ty * 4, HM, am);
-            lds_frag<BK, LDA>(cA, 1, kk, ty * 4, HM, mm);
+            uint32_t aa[8], bb[8];
+            lds_frag<BK, LDA>(cA, 2, kk, ty * 4, HM, aa);
             lds_frag<BK, LDB>(cB, 0, kk, tx * 4, HN, bb);
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const uint32_t a = mm[i] | (am[i] & kMant);
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
-                    acc[i][j] += __uint_as_float(pam_full(a, bb[j] + kBias));
+                    acc[i][j] += __uint_as_float(pam_full(aa[i], bb[j] + kBias));
             }
         }
     }

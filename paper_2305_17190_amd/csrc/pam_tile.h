@@ -131,10 +131,10 @@ struct TileLoader {
         }
     }
 
-    // Scan the held elements.  Returns bit 0 when some element is "tiny" (a
-    // normal number with exponent field 1..63, whose products can
-    // underflow) and bit 1 when some element needs the SPECIAL path (inf, NaN
-    // or |x| >= 2^64).  Zeros and denormals are neither.
+    // Scan the held elements.  Returns bit 0 when some element has exponent
+    // field below 64 (zero, denormal, or "tiny": a normal number whose
+    // products can underflow) and bit 1 when some element needs the SPECIAL
+    // path (inf, NaN or |x| >= 2^64).
     __device__ __forceinline__ uint32_t scan() const {
         uint32_t hi = 0, lo = 0xFFFFFFFFu;
 #pragma unroll
@@ -144,24 +144,21 @@ struct TileLoader {
             for (int c = 0; c < 4; ++c) {
                 const uint32_t ex = e[c] & kExpMask;
                 hi = max(hi, ex);
-                lo = min(lo, ex - kMinNormal);   // a zero field wraps to the top
+                lo = min(lo, ex);
             }
         }
-        return (lo < (63u << 23) ? 1u : 0u) | (hi >= (191u << 23) ? 2u : 0u);
-    }
-
-    // "Tiny": a normal number with exponent field 1..63.
-    __device__ __forceinline__ static bool tiny(uint32_t u) {
-        return (u & kExpMask) - kMinNormal < (63u << 23);
+        return (lo < (64u << 23) ? 1u : 0u) | (hi >= (191u << 23) ? 2u : 0u);
     }
 
     // Write the chunk into LDS buffer s, k-major: s[plane][kk][o].  A: plane 0
-    // aM (1 + M), plane 1 m (+-2^E or +-0); B: plane 0 b' (b - bias, zero and
-    // denormal b as a signed zero first).  When `has_tiny`, a tiny element at
-    // chunk step k sets bit k % 16 of mask[(k / 16) * (b_slot + 1) + w], w
-    // being the row wave that reads it (A) or b_slot (B).
+    // aM (1 + M), plane 1 m (+-2^E or +-0), plane 2 a itself; B: plane 0 b'
+    // (b - bias, zero and denormal b as a signed zero first).  When
+    // `has_low`, an element at chunk step k with exponent field below 64 sets
+    // bit k % 16 of mask[(k / 16) * (b_slot + 1) + w], and a normal one among
+    // them (tiny) also bit 16 + k % 16; w is the row wave that reads the
+    // element (A) or b_slot (B).
     template <int LDS_LD, typename RowWave>
-    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], bool is_b, int tid, bool has_tiny,
+    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], bool is_b, int tid, bool has_low,
                                           uint32_t *mask, int b_slot, RowWave row_wave) const {
 #pragma unroll
         for (int r = 0; r < L; ++r) {
@@ -193,19 +190,26 @@ struct TileLoader {
 #pragma unroll
                     for (int c = 0; c < 4; ++c)
                         s[1][kk + c][o] = p1[c];
+#pragma unroll
+                    for (int c = 0; c < 4; ++c)
+                        s[2][kk + c][o] = e[c];
                 }
             } else {
                 *reinterpret_cast<uint4 *>(&s[0][kk][o]) = make_uint4(p0[0], p0[1], p0[2], p0[3]);
-                if (!is_b)
+                if (!is_b) {
                     *reinterpret_cast<uint4 *>(&s[1][kk][o]) = make_uint4(p1[0], p1[1], p1[2], p1[3]);
+                    *reinterpret_cast<uint4 *>(&s[2][kk][o]) = v[r];
+                }
             }
-            if (has_tiny) {
+            if (has_low) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
-                    if (tiny(e[c])) {
+                    const uint32_t ex = e[c] & kExpMask;
+                    if (ex < (64u << 23)) {
                         const int k = KCONTIG ? kk + c : kk;
+                        const uint32_t bit = 1u << (k % 16);
                         atomicOr(&mask[(k / 16) * (b_slot + 1) + (is_b ? b_slot : row_wave(KCONTIG ? o : o + c))],
-                                 1u << (k % 16));
+                                 ex != 0u ? (bit | (bit << 16)) : bit);
                     }
                 }
             }

@@ -134,14 +134,19 @@ pam_status_t pam_gemm_batched(pam_op_t transA, pam_op_t transB, int64_t m, int64
 /*
  * How a product is tiled: output tile tile_m x tile_n per workgroup;
  * kgroups waves per micro-tile position that share each LDS chunk's k steps
- * and add their partial tiles in LDS; and the number of K slices whose
- * partial sums are added by a second kernel (1 = none).
+ * and add their partial tiles in LDS; the number of K slices whose partial
+ * sums are added by a second kernel (1 = none); and with splits > 1, how many
+ * tiles take the whole K in the same launch instead: the first whole_tiles
+ * tiles, numbered batch-major, then by tile row, then tile column (0 = every
+ * tile is split; >= the tile count = none is).  Splitting only the last
+ * tiles fills the last round of workgroups with shorter ones.
  */
 typedef struct {
     int32_t tile_m;
     int32_t tile_n;
     int32_t splits;
     int32_t kgroups;
+    int64_t whole_tiles;
 } pam_plan_t;
 
 /* The plan pam_gemm / pam_gemm_batched would use for these sizes. */
@@ -150,8 +155,10 @@ pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_p
 /*
  * pam_gemm_batched with an explicit plan (for tests and tuning).
  * (tile_m, tile_n, kgroups) is (128,128,1), (128,64,1), (64,64,1) or
- * (64,64,4); 1 <= splits <= 64.  The result is the same product as with
- * the automatic plan, up to float32 summation order.
+ * (64,64,4); 1 <= splits <= 64; whole_tiles >= 0.  The result is the same
+ * product as with the automatic plan, up to float32 summation order.  A plan
+ * with 0 < whole_tiles < tiles runs as one launch and fails with
+ * PAM_ERROR_INVALID_VALUE when its workgroups exceed 2^24 - 1.
  */
 pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB,
                                         int64_t m, int64_t n, int64_t k,

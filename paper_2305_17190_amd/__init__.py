@@ -41,7 +41,7 @@ class PamError(RuntimeError):
 
 class _Plan(ctypes.Structure):
     _fields_ = [("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32), ("splits", ctypes.c_int32),
-                ("kgroups", ctypes.c_int32)]
+                ("kgroups", ctypes.c_int32), ("whole_tiles", ctypes.c_int64)]
 
 
 class _DeviceInfo(ctypes.Structure):
@@ -221,8 +221,9 @@ def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, mantissa_
 def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None, mantissa_bits: int = 23):
     """Batched C[z] = op(A[z]) .^ op(B[z]) over the leading axis.
 
-    ``plan`` = (tile_m, tile_n, splits[, kgroups]) forces a tiling (tests
-    and tuning).  ``mantissa_bits`` < 23 rounds every operand element to that
+    ``plan`` = (tile_m, tile_n, splits[, kgroups[, whole_tiles]]) forces a
+    tiling (tests and tuning); ``whole_tiles`` tiles, counted from the first,
+    then take the whole K and only the rest are split.  ``mantissa_bits`` < 23 rounds every operand element to that
     many mantissa bits first (the library then picks the plan).
     """
     torch = _torch()
@@ -250,7 +251,10 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
     elif plan is None:
         _check(lib.pam_gemm_batched(*args, _stream_handle(A)))
     else:
-        p = _Plan(*plan) if len(plan) == 4 else _Plan(plan[0], plan[1], plan[2], 1)
+        if not 3 <= len(plan) <= 5:
+            raise ValueError("plan is (tile_m, tile_n, splits[, kgroups[, whole_tiles]])")
+        full = tuple(plan) + (1, 0)[len(plan) - 3:]
+        p = _Plan(*full)
         _check(lib.pam_gemm_batched_with_plan(*args, ctypes.byref(p), _stream_handle(A)))
     return out
 
@@ -282,10 +286,11 @@ def exact_grad(A, B, Mod, trans_a: bool = False, out=None):
 
 
 def plan(m: int, n: int, k: int, batch: int = 1):
-    """(tile_m, tile_n, splits, kgroups) the library picks for these sizes."""
+    """(tile_m, tile_n, splits, kgroups, whole_tiles) the library picks for
+    these sizes."""
     p = _Plan()
     _check(load().pam_gemm_plan(m, n, k, batch, ctypes.byref(p)))
-    return (p.tile_m, p.tile_n, p.splits, p.kgroups)
+    return (p.tile_m, p.tile_n, p.splits, p.kgroups, p.whole_tiles)
 
 
 def device_info(device: int = 0) -> dict:

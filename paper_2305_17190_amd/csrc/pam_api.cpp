@@ -35,9 +35,13 @@ constexpr int64_t kMaxSplits = 64;
 // 128 rows of a panel, in bytes, must fit the kernels' 32-bit offsets.
 constexpr int64_t kMaxLd = (int64_t)1 << 22;
 
+// With splits > 1, the first whole_tiles tiles (batch-major, then tile row,
+// then tile column) take the whole K and the rest are split into `splits` K
+// slices of k_per_split; whole_tiles == 0: every tile is split.
 struct Plan {
     int tile_m, tile_n, kgroups, splits;
     int64_t k_per_split;
+    int64_t whole_tiles;
 };
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -52,25 +56,35 @@ struct Shape {
 // k-group, or whose four waves split each chunk's k steps (four times the
 // waves without partial sums in HBM, at twice the staging work per MAC).
 // The 128 x 128 tile holds three waves per SIMD, the others two.
-const Shape kShapes[] = {{128, 128, 1, 4, 3, 24.3e12},
-                         {128, 64, 1, 2, 4, 19.5e12},
-                         {64, 64, 1, 1, 8, 18.1e12},
-                         {64, 64, 4, 4, 2, 17.2e12}};
+const Shape kShapes[] = {{128, 128, 1, 4, 3, 26.67e12},
+                         {128, 64, 1, 2, 4, 20.49e12},
+                         {64, 64, 1, 1, 8, 19.64e12},
+                         {64, 64, 4, 4, 2, 15.99e12}};
 constexpr int kComputeUnits = 256;
 constexpr int kSimdsPerCu = 4;
 // Vector-ALU throughput of one SIMD holding 0..3 waves of this kernel,
 // relative to three: one wave issues alone, two pair their adds and fmas
 // but leave barrier and LDS waits exposed.
-constexpr double kSimdEfficiency[4] = {0.0, 0.421, 0.808, 1.0};
-constexpr double kWorkgroupFixedS = 3.4e-6;  // first loads, epilogue stores
-constexpr double kSplitFixedS = 9.6e-6;      // second launch
-constexpr double kPartialBytesPerS = 7.1e12; // writing and re-reading partial sums
+constexpr double kSimdEfficiency[4] = {0.0, 0.4132, 0.8558, 1.0};
+constexpr double kWorkgroupFixedS = 5.0e-6;  // first loads, epilogue stores
+constexpr double kSplitFixedS = 9.0e-6;      // second launch, workspace
+// Effective rate of writing and re-reading partial sums: up to a few hundred
+// MB they largely stay in the last-level cache, so above the HBM rate.
+constexpr double kPartialBytesPerS = 9.6e12;
 // Workgroups start as soon as slots free up, so a partial last round costs
 // less than a full one the more rounds precede it (they end staggered).
-constexpr double kTailDamping = 0.457;
+constexpr double kTailDamping = 0.4829;
+// Compute units run at different clocks under load, so the last round of
+// workgroups does not end at once: the launch ends this fraction of one
+// workgroup's duration after the average, scaled by how many slots the last
+// round leaves without a shorter partial-round workgroup to absorb it.
+constexpr double kRoundImbalance = 0.0788;
 // Split-K plans must beat the best unsplit plan by this factor (they change
 // the summation order and take a workspace).
 constexpr double kSplitMargin = 0.97;
+// Plans with whole-K tiles beside split ones run in one launch; the planner
+// offers them up to this many tiles.
+constexpr int64_t kMaxHybridTiles = 1 << 20;
 // Split counts the plan search considers.
 constexpr int kSplitChoices[] = {1, 2, 3, 4, 5, 6, 7, 8, 12, 16, 24, 32, 48, 64};
 
@@ -81,26 +95,23 @@ double cu_efficiency(int waves_per_cu) {
            kSimdsPerCu;
 }
 
-Plan make_plan(const Shape &c, int64_t k, int64_t splits) {
-    Plan p{c.bm, c.bn, c.kw, 1, k};
+Plan make_plan(const Shape &c, int64_t k, int64_t splits, int64_t whole_tiles = 0) {
+    Plan p{c.bm, c.bn, c.kw, 1, k, 0};
     if (splits > 1) {
         const int64_t per = ceil_div(ceil_div(k, splits), pamk::kChunkK * c.kw) * pamk::kChunkK * c.kw;
         p.k_per_split = per;
         p.splits = (int)ceil_div(k, per);
+        p.whole_tiles = p.splits > 1 ? whole_tiles : 0;
     }
     return p;
 }
 
-// Estimated time: full rounds of resident workgroups at the shape's rate,
-// then a partial round whose workgroups share compute units with fewer
-// others (faster each, slower in total), plus for split-K a second launch
-// and the partial sums' round trip through memory.
-double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t batch) {
-    const int64_t bk = pamk::kChunkK * c.kw;
-    const int64_t chunks = ceil_div(p.k_per_split, bk);
-    const int64_t wgs = ceil_div(m, c.bm) * ceil_div(n, c.bn) * batch * p.splits;
+// Time of `wgs` workgroups of wg_s seconds each, dispatched after `before`
+// full rounds of others: full rounds at the shape's rate, then a partial
+// round whose workgroups share compute units with fewer others (faster each,
+// slower in total), then the uneven end of the last round.
+double rounds_time(const Shape &c, int64_t wgs, double wg_s, int64_t before) {
     const int64_t slots = (int64_t)c.per_cu * kComputeUnits;
-    const double wg_s = double(c.bm) * c.bn * bk * chunks * slots / c.rate + kWorkgroupFixedS;
     const int64_t rounds = wgs / slots;
     const int64_t rest = wgs % slots;
     double t = double(rounds) * wg_s;
@@ -109,31 +120,66 @@ double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t ba
         const double partial = wg_s * (double(q) / c.per_cu) * cu_efficiency(c.per_cu * c.waves) /
                                cu_efficiency(q * c.waves);
         const double even = wg_s * double(rest) / double(slots);
-        t += even + (partial - even) / (1.0 + kTailDamping * double(rounds));
+        t += even + (partial - even) / (1.0 + kTailDamping * double(before + rounds));
     }
-    if (p.splits > 1)
-        t += kSplitFixedS + double(p.splits + 1) * double(m) * double(n) * double(batch) * 4.0 / kPartialBytesPerS;
+    if (before + rounds > 0)
+        t += kRoundImbalance * wg_s * (1.0 - double(rest) / double(slots));
     return t;
 }
 
-// The cheapest (shape, split) by plan_time; splits keep at least four
-// chunks each.
+// Estimated time of a plan: the whole-K tiles (a whole number of rounds in
+// the plans considered), then the K slices of the split tiles, plus for
+// split-K a second launch and the partial sums' round trip through memory.
+double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t k, int64_t batch) {
+    const int64_t bk = pamk::kChunkK * c.kw;
+    const int64_t slots = (int64_t)c.per_cu * kComputeUnits;
+    const int64_t tiles = ceil_div(m, c.bm) * ceil_div(n, c.bn) * batch;
+    const double per_chunk = double(c.bm) * c.bn * bk * slots / c.rate;
+    const double wg_whole = per_chunk * double(ceil_div(k, bk)) + kWorkgroupFixedS;
+    if (p.splits <= 1)
+        return rounds_time(c, tiles, wg_whole, 0);
+    const int64_t whole = std::min(p.whole_tiles, tiles);
+    const int64_t split_tiles = tiles - whole;
+    const int64_t before = whole / slots;
+    const double wg_slice = per_chunk * double(ceil_div(p.k_per_split, bk)) + kWorkgroupFixedS;
+    double t = double(before) * wg_whole + rounds_time(c, split_tiles * p.splits, wg_slice, before);
+    t += kSplitFixedS + double(p.splits + 1) * double(split_tiles) * c.bm * c.bn * 4.0 / kPartialBytesPerS;
+    return t;
+}
+
+// The cheapest plan by plan_time: for each tile shape every split count
+// (slices of at least four chunks), and, when the tiles leave a partial last
+// round, split counts for just that round's tiles (or those of the last
+// round and a half) while the rest take the whole K.  A plan with split-K
+// must beat the best unsplit one by kSplitMargin.
 Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch) {
     double best_t[2] = {0.0, 0.0};
     Plan best[2] = {};
     bool have[2] = {false, false};
+    auto consider = [&](const Shape &c, const Plan &p) {
+        const double t = plan_time(c, p, m, n, k, batch);
+        const int split = p.splits > 1 ? 1 : 0;
+        if (!have[split] || t < best_t[split]) {
+            best_t[split] = t;
+            best[split] = p;
+            have[split] = true;
+        }
+    };
     for (const auto &c : kShapes) {
         const int64_t most = std::max<int64_t>(1, std::min(kMaxSplits, k / (4 * pamk::kChunkK * c.kw)));
+        const int64_t slots = (int64_t)c.per_cu * kComputeUnits;
+        const int64_t tiles = ceil_div(m, c.bm) * ceil_div(n, c.bn) * batch;
+        const int64_t rest = tiles % slots;
         for (const int s : kSplitChoices) {
             if (s > most)
                 break;
-            const Plan p = make_plan(c, k, s);
-            const double t = plan_time(c, p, m, n, batch);
-            const int split = p.splits > 1 ? 1 : 0;
-            if (!have[split] || t < best_t[split]) {
-                best_t[split] = t;
-                best[split] = p;
-                have[split] = true;
+            consider(c, make_plan(c, k, s));
+            if (s == 1 || rest == 0 || tiles <= slots)
+                continue;
+            for (const int64_t tail : {rest, rest + slots}) {
+                if (tail >= tiles || tiles > kMaxHybridTiles)
+                    continue;
+                consider(c, make_plan(c, k, s, tiles - tail));
             }
         }
     }
@@ -233,17 +279,34 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     p.n = (int32_t)n;
     p.k = (int32_t)k;
     p.k_per_split = (int32_t)std::min<int64_t>(plan.k_per_split, kMaxDim);
-    p.splits = plan.splits;
     p.tiles_n = (int32_t)ceil_div(n, plan.tile_n);
     p.vec_a = aligned16(A) && lda % 4 == 0 && (batch == 1 || sa % 4 == 0);
     p.vec_b = aligned16(B) && ldb % 4 == 0 && (batch == 1 || sb % 4 == 0);
+    p.vec_c = aligned16(C) && ldc % 4 == 0 && (batch == 1 || sc % 4 == 0);
     p.round_drop = round_drop;
 
-    const int64_t gz_max = kMaxGridZ;
+    // Work items per launch: whole-K tiles, then `splits` slices of each
+    // split tile.  A plan with whole-K tiles beside split ones runs as one
+    // launch; otherwise launches take as many whole matrices as fit.
+    const int64_t tiles = ceil_div(m, plan.tile_m) * p.tiles_n;
+    const int64_t total = tiles * batch;
+    int64_t splits = plan.splits > 1 ? plan.splits : 1;
+    if (plan.whole_tiles >= total)
+        splits = 1;
+    const int64_t whole_tiles = splits > 1 ? plan.whole_tiles : 0;
+    const bool hybrid = whole_tiles > 0;
+    if (tiles > kMaxDim || tiles * splits > pamk::kMaxLaunchItems ||
+        (hybrid && whole_tiles + (total - whole_tiles) * splits > pamk::kMaxLaunchItems))
+        return fail(PAM_ERROR_INVALID_VALUE, "too many workgroups for one launch (output too large for the plan)");
+    const int64_t per_launch = hybrid ? batch : std::max<int64_t>(1, pamk::kMaxLaunchItems / (tiles * splits));
+    p.tiles = (int32_t)tiles;
+    p.splits = (int32_t)splits;
+
     float *ws = nullptr;
-    if (plan.splits > 1) {
-        const int64_t nb = std::min(batch, gz_max);
-        const size_t bytes = (size_t)nb * plan.splits * (size_t)m * (size_t)n * sizeof(float);
+    const int64_t ws_tiles = hybrid ? total - whole_tiles : (splits > 1 ? std::min(batch, per_launch) * tiles : 0);
+    if (ws_tiles > 0) {
+        const size_t bytes = (size_t)splits * (size_t)ws_tiles * (size_t)plan.tile_m * (size_t)plan.tile_n *
+                             sizeof(float);
         hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), bytes, stream);
         if (e != hipSuccess || ws == nullptr) {
             g_last_error = std::string("hipMallocAsync of the split-K workspace: ") + hipGetErrorString(e);
@@ -251,21 +314,30 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
         }
     }
     pam_status_t result = PAM_SUCCESS;
-    for (int64_t b0 = 0; b0 < batch && result == PAM_SUCCESS; b0 += gz_max) {
-        const int64_t nb = std::min(gz_max, batch - b0);
+    for (int64_t b0 = 0; b0 < batch && result == PAM_SUCCESS; b0 += per_launch) {
+        const int64_t nb = std::min(per_launch, batch - b0);
         p.A = A + b0 * sa;
         p.B = B + b0 * sb;
         p.C = C + b0 * sc;
         p.W = ws;
-        p.vec_c = ws ? (n % 4 == 0) : (aligned16(C) && ldc % 4 == 0 && (batch == 1 || sc % 4 == 0));
+        if (hybrid) {
+            p.whole = (int32_t)whole_tiles;
+            p.split_tiles = (int32_t)(total - whole_tiles);
+        } else if (splits > 1) {
+            p.whole = 0;
+            p.split_tiles = (int32_t)(nb * tiles);
+        } else {
+            p.whole = (int32_t)(nb * tiles);
+            p.split_tiles = 0;
+        }
         hipError_t e = pamk::launch_pam_gemm(plan.tile_m, plan.tile_n, plan.kgroups, ta == PAM_OP_T, tb == PAM_OP_T, p,
-                                             nb, stream);
+                                             stream);
         if (e != hipSuccess) {
             result = fail_hip(e, "gemm kernel launch");
             break;
         }
-        if (ws) {
-            e = pamk::launch_splitk_reduce(ws, p.C, (int32_t)m, (int32_t)n, ldc, sc, plan.splits, nb, stream);
+        if (p.split_tiles > 0) {
+            e = pamk::launch_split_tile_reduce(plan.tile_m, plan.tile_n, p, stream);
             if (e != hipSuccess)
                 result = fail_hip(e, "split-K reduce launch");
         }
@@ -513,6 +585,7 @@ pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_p
     plan->tile_n = p.tile_n;
     plan->splits = p.splits;
     plan->kgroups = p.kgroups;
+    plan->whole_tiles = p.whole_tiles;
     return PAM_SUCCESS;
 }
 
@@ -534,13 +607,16 @@ pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB, int64_
                     "(tile_m, tile_n, kgroups) must be (128,128,1), (128,64,1), (64,64,1) or (64,64,4)");
     if (plan->splits < 1 || plan->splits > kMaxSplits)
         return fail(PAM_ERROR_INVALID_VALUE, "splits must be in [1, 64]");
+    if (plan->whole_tiles < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "whole_tiles must be >= 0");
     if (m == 0 || n == 0 || batch == 0)
         return PAM_SUCCESS;
-    Plan p{plan->tile_m, plan->tile_n, plan->kgroups, 1, std::max<int64_t>(k, 1)};
+    Plan p{plan->tile_m, plan->tile_n, plan->kgroups, 1, std::max<int64_t>(k, 1), 0};
     if (plan->splits > 1 && k > 0) {
         const int64_t per = ceil_div(ceil_div(k, plan->splits), pamk::kChunkK) * pamk::kChunkK;
         p.k_per_split = per;
         p.splits = (int)ceil_div(k, per);
+        p.whole_tiles = plan->whole_tiles;
     }
     return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch, p, stream);
 }

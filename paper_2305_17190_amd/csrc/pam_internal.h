@@ -11,17 +11,27 @@ namespace pamk {
 constexpr int kChunkK = 16;
 
 // Arguments of one (batched, possibly split-K) PAM matrix product launch.
+//
+// Matrix product launches run whole + split_tiles * splits work items: tiles
+// are numbered batch-major, then by tile row, then tile column (`tiles` per
+// matrix, `tiles_n` per tile row); item i < whole computes tile i over the
+// whole K into C; item whole + s * split_tiles + t computes K slice s (k in
+// [s * k_per_split, (s + 1) * k_per_split)) of tile whole + t into the
+// tile-packed partial sums W[s][t][tile_m][tile_n].
 struct GemmParams {
     const float *A;
     const float *B;
-    float *C;          // final output (used when W == nullptr)
-    float *W;          // split-K partial sums [batch][splits][m][n], or nullptr
+    float *C;          // final output
+    float *W;          // partial sums of the split tiles, or nullptr (layout per kernel)
     int64_t lda, ldb, ldc;
     int64_t strideA, strideB, strideC;
     int32_t m, n, k;
     int32_t k_per_split;  // multiple of kChunkK
     int32_t splits;
     int32_t tiles_n;
+    int32_t tiles;        // matrix products: tiles per matrix
+    int32_t whole;        // matrix products: whole-K work items
+    int32_t split_tiles;  // matrix products: tiles split into `splits` K slices
     int32_t vec_a;        // float4 global loads of A are aligned
     int32_t vec_b;        // float4 global loads of B are aligned
     int32_t vec_c;        // float4 stores of the output are aligned
@@ -42,15 +52,24 @@ hipError_t launch_paexp2(const float *a, float *out, int64_t n, hipStream_t stre
 hipError_t launch_round_mantissa(const float *a, float *out, int64_t n, int drop, hipStream_t stream);
 
 // (tile_m, tile_n, kgroups) in {(128,128,1), (128,64,1), (64,64,1), (64,64,4)};
-// grid = (tiles_m * tiles_n, splits, batch_in_launch).
+// a one-dimensional grid of p.whole + p.split_tiles * p.splits workgroups.
 hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b,
-                           const GemmParams &p, int64_t batch, hipStream_t stream);
+                           const GemmParams &p, hipStream_t stream);
+
+// C of the split tiles of a matrix product launch: element by element the sum
+// over s = 0, 1, ... of W[s][t][.][.], in that order.
+hipError_t launch_split_tile_reduce(int tile_m, int tile_n, const GemmParams &p, hipStream_t stream);
+
+// Workgroups one matrix product launch may hold (its grid, in threads, stays
+// below 2^32).
+constexpr int64_t kMaxLaunchItems = 16777215;
 
 // Exact-derivative product (pam_exact_grad.hip): C(r, c) = sum_q op(A)(r, q)
 // d(B(q, c) .^ Mod(r, c)) / dB(q, c); 128 x 128 tiles, grid (tiles, splits).
 hipError_t launch_pam_exact_grad(bool trans_a, const GemmParams &p, hipStream_t stream);
 
-// C[b][i][j] = sum_s W[b][s][i][j], s in increasing order.
+// Exact-derivative products: C[b][i][j] = sum_s W[b][s][i][j], s in
+// increasing order.
 hipError_t launch_splitk_reduce(const float *W, float *C, int32_t m, int32_t n, int64_t ldc,
                                 int64_t strideC, int32_t splits, int64_t batch, hipStream_t stream);
 

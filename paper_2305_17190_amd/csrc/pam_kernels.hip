@@ -288,14 +288,23 @@ pam_gemm_kernel(GemmParams p) {
     const int ty = t / TXN;
     const int wave = tid >> 6;
     const int rwave = t >> 6;
-    const int tm = blockIdx.x / p.tiles_n;
-    const int tn = blockIdx.x % p.tiles_n;
+    // Work item -> (tile, K range): whole-K tiles first, then the K slices of
+    // the split tiles, slice by slice (neighbouring items share operand rows).
+    const uint32_t item = blockIdx.x;
+    const bool whole = item < (uint32_t)p.whole;
+    const uint32_t rel = item - (uint32_t)p.whole;
+    const uint32_t nsplit = (uint32_t)max(p.split_tiles, 1);
+    const uint32_t st = whole ? 0u : rel % nsplit;
+    const int split = whole ? 0 : (int)(rel / nsplit);
+    const uint32_t tile_lin = whole ? item : (uint32_t)p.whole + st;
+    const int64_t bz = tile_lin / (uint32_t)p.tiles;
+    const int tile = (int)(tile_lin % (uint32_t)p.tiles);
+    const int tm = tile / p.tiles_n;
+    const int tn = tile % p.tiles_n;
     const int m0 = tm * BM;
     const int n0 = tn * BN;
-    const int split = blockIdx.y;
-    const int64_t bz = blockIdx.z;
-    const int kb = split * p.k_per_split;
-    const int ke = min(p.k, kb + p.k_per_split);
+    const int kb = whole ? 0 : split * p.k_per_split;
+    const int ke = whole ? p.k : min(p.k, kb + p.k_per_split);
     const int nchunks = ke > kb ? (ke - kb + BK - 1) / BK : 0;
 
     // Chunk bases (uniform): op(A) rows m0.., op(B) columns n0.., at k = kb.
@@ -421,33 +430,42 @@ pam_gemm_kernel(GemmParams p) {
         }
     }
 
-    // Epilogue: final output, or this split's slice of the partial sums.
+    // Epilogue: the output tile in C, or this K slice's partial tile (packed,
+    // written whole: rows and columns past the output are never read).
     float *out;
     int64_t ld;
-    if (p.W != nullptr) {
-        out = p.W + ((bz * p.splits + split) * (int64_t)p.m) * p.n;
-        ld = p.n;
-    } else {
-        out = p.C + bz * p.strideC;
+    int lim_m, lim_n;
+    bool vec;
+    if (whole) {
+        out = p.C + bz * p.strideC + (int64_t)m0 * p.ldc + n0;
         ld = p.ldc;
+        lim_m = p.m - m0;
+        lim_n = p.n - n0;
+        vec = p.vec_c != 0;
+    } else {
+        out = p.W + ((int64_t)split * p.split_tiles + st) * (BM * BN);
+        ld = BN;
+        lim_m = BM;
+        lim_n = BN;
+        vec = true;
     }
     if (KW == 1) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            const int row = m0 + (i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4));
-            if (row >= p.m)
+            const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+            if (row >= lim_m)
                 continue;
             float *orow = out + (int64_t)row * ld;
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const int col = n0 + (h == 0 ? tx * 4 : HN + tx * 4);
-                if (p.vec_c && col + 3 < p.n) {
+                const int col = h == 0 ? tx * 4 : HN + tx * 4;
+                if (vec && col + 3 < lim_n) {
                     *reinterpret_cast<float4 *>(orow + col) =
                         make_float4(acc[i][4 * h], acc[i][4 * h + 1], acc[i][4 * h + 2], acc[i][4 * h + 3]);
                 } else {
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        if (col + j < p.n)
+                        if (col + j < lim_n)
                             orow[col + j] = acc[i][4 * h + j];
                 }
             }
@@ -475,9 +493,8 @@ pam_gemm_kernel(GemmParams p) {
         const int e0 = tid * PER;
         const int row = e0 / BN;
         const int col0 = e0 % BN;
-        const int grow = m0 + row;
-        if (grow < p.m) {
-            float *orow = out + (int64_t)grow * ld;
+        if (row < lim_m) {
+            float *orow = out + (int64_t)row * ld;
 #pragma unroll
             for (int q = 0; q < PER / 4; ++q) {
                 const int col = col0 + 4 * q;
@@ -490,15 +507,14 @@ pam_gemm_kernel(GemmParams p) {
                     sum.z += x.z;
                     sum.w += x.w;
                 }
-                const int gcol = n0 + col;
-                if (p.vec_c && gcol + 3 < p.n) {
-                    *reinterpret_cast<float4 *>(orow + gcol) = sum;
+                if (vec && col + 3 < lim_n) {
+                    *reinterpret_cast<float4 *>(orow + col) = sum;
                 } else {
                     const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        if (gcol + j < p.n)
-                            orow[gcol + j] = sv[j];
+                        if (col + j < lim_n)
+                            orow[col + j] = sv[j];
                 }
             }
         }
@@ -520,9 +536,11 @@ static hipError_t launch_tile(bool ta, bool tb, const GemmParams &p, dim3 grid, 
 }
 
 hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, const GemmParams &p,
-                           int64_t batch, hipStream_t stream) {
-    const int64_t tiles_m = (p.m + tile_m - 1) / tile_m;
-    const dim3 grid((unsigned)(tiles_m * p.tiles_n), (unsigned)p.splits, (unsigned)batch);
+                           hipStream_t stream) {
+    const int64_t items = (int64_t)p.whole + (int64_t)p.split_tiles * p.splits;
+    if (items <= 0 || items > kMaxLaunchItems)
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)items);
     if (tile_m == 128 && tile_n == 128 && kgroups == 1)
         return launch_tile<128, 128, 1>(trans_a, trans_b, p, grid, stream);
     if (tile_m == 128 && tile_n == 64 && kgroups == 1)
@@ -554,6 +572,57 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(const float *__restr
             s += w[q * mn];
         C[b * strideC + i * ldc + j] = s;
     }
+}
+
+// Each workgroup adds the K slices of a 256 x 4-output part of one split
+// tile (grid-stride over the parts); each thread four consecutive outputs,
+// slice by slice.
+__global__ void __launch_bounds__(256) split_tile_reduce_kernel(GemmParams p, int bm, int bn) {
+    const int gpr = bn / 4;                      // four-output groups per tile row
+    const int parts = bm * bn / 4 / 256;         // parts per tile
+    const int64_t tile_elems = (int64_t)bm * bn;
+    const int64_t slice = (int64_t)p.split_tiles * tile_elems;
+    const int64_t nparts = (int64_t)p.split_tiles * parts;
+    for (int64_t b = blockIdx.x; b < nparts; b += gridDim.x) {
+        const int64_t t = b / parts;
+        const int g = (int)(b % parts) * 256 + threadIdx.x;
+        const int64_t tile_lin = p.whole + t;
+        const int64_t bz = tile_lin / p.tiles;
+        const int tile = (int)(tile_lin % p.tiles);
+        const int m0 = (tile / p.tiles_n) * bm;
+        const int n0 = (tile % p.tiles_n) * bn;
+        const int r = g / gpr;
+        const int c = (g % gpr) * 4;
+        if (m0 + r >= p.m || n0 + c >= p.n)
+            continue;
+        const float *w = p.W + t * tile_elems + r * bn + c;
+        float4 sum = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        for (int q = 0; q < p.splits; ++q) {
+            const float4 x = *reinterpret_cast<const float4 *>(w + q * slice);
+            sum.x += x.x;
+            sum.y += x.y;
+            sum.z += x.z;
+            sum.w += x.w;
+        }
+        float *crow = p.C + bz * p.strideC + (int64_t)(m0 + r) * p.ldc + n0;
+        if (p.vec_c && n0 + c + 3 < p.n) {
+            *reinterpret_cast<float4 *>(crow + c) = sum;
+        } else {
+            const float sv[4] = {sum.x, sum.y, sum.z, sum.w};
+            for (int j = 0; j < 4; ++j)
+                if (n0 + c + j < p.n)
+                    crow[c + j] = sv[j];
+        }
+    }
+}
+
+hipError_t launch_split_tile_reduce(int tile_m, int tile_n, const GemmParams &p, hipStream_t stream) {
+    if (p.split_tiles <= 0)
+        return hipSuccess;
+    const int64_t parts = (int64_t)p.split_tiles * (tile_m * tile_n / 4 / 256);
+    const int64_t blocks = std::min<int64_t>(parts, 256 * 32);
+    hipLaunchKernelGGL(split_tile_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, p, tile_m, tile_n);
+    return hipGetLastError();
 }
 
 hipError_t launch_splitk_reduce(const float *W, float *C, int32_t m, int32_t n, int64_t ldc, int64_t strideC,

@@ -98,29 +98,34 @@ def test_elementwise_rejects_null_pointers(lib):
 
 def test_plan_selection_is_host_logic(lib):
     # Large products use the 128x128 tile (three workgroups per compute
-    # unit, 768 slots); with 4096 tiles the last partial round is cheap and
-    # K stays whole.
-    assert pam.plan(16384, 4096, 4096) == (128, 128, 1, 1)
+    # unit, 768 slots); 4096 tiles are five full rounds and 256 more: those
+    # last tiles are K-split so they fill the last round, the rest keep K
+    # whole.
+    tm, tn, s, kg, whole = pam.plan(16384, 4096, 4096)
+    assert (tm, tn, kg) == (128, 128, 1) and s > 1 and whole == 5 * 768
     # 1024 tiles on 768 slots would leave a last round on a third of the
-    # slots: K is split so the workgroups fill whole rounds.
-    tm, tn, s, kg = pam.plan(4096, 4096, 16384)
-    assert (tm, tn, kg) == (128, 128, 1) and 2 <= s <= 8
+    # slots: K is split (for every tile, or for the last round's tiles while
+    # the first round takes the whole K) so the workgroups fill whole rounds.
+    tm, tn, s, kg, whole = pam.plan(4096, 4096, 16384)
+    assert (tm, tn, kg) == (128, 128, 1) and 2 <= s <= 16 and whole in (0, 768)
     assert pam.plan(8192, 2048, 512)[:2] == (128, 128)
-    # Narrow outputs with long K split K; short-K batched narrow outputs use
-    # the 64x64 tile whose four waves share each chunk's k steps.
+    # Narrow outputs with long K split K; short-K batched narrow outputs get
+    # more workgroups than 128x128 tiles would give (smaller tiles, K slices
+    # or k-groups).
     assert pam.plan(8192, 512, 2048)[2] > 1
     assert pam.plan(768, 192, 12608)[2] >= 16
-    assert pam.plan(256, 64, 256, 256) == (64, 64, 1, 4)
+    tm, tn, s, kg, whole = pam.plan(256, 64, 256, 256)
+    assert (tm, tn) != (128, 128) and (s > 1 or kg > 1)
     for m, n, k, b in ((1, 1, 1, 1), (5, 7, 3, 1), (300, 1, 17, 1), (16, 16, 100000, 1), (64, 64, 0, 3)):
-        tm, tn, s, kg = pam.plan(m, n, k, b)
+        tm, tn, s, kg, whole = pam.plan(m, n, k, b)
         assert (tm, tn, kg) in ((128, 128, 1), (128, 64, 1), (64, 64, 1), (64, 64, 4))
-        assert 1 <= s <= 64
+        assert 1 <= s <= 64 and whole >= 0
     with pytest.raises(pam.PamError):
         pam.plan(0, 4, 4)
 
 
 @pytest.mark.parametrize("plan", [(96, 64, 1, 1), (128, 128, 0, 1), (128, 128, 1, 4), (64, 64, 1, 2),
-                                  (64, 64, 65, 1)])
+                                  (64, 64, 65, 1), (128, 128, 2, 1, -1)])
 def test_with_plan_rejects_bad_tiles(lib, plan):
     P = pam._Plan(*plan)
     assert lib.pam_gemm_batched_with_plan(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1, ctypes.byref(P), None) == 1

@@ -16,7 +16,9 @@ from oracle import pam_ref
 pytestmark = pytest.mark.gpu
 
 PLANS = [(128, 128, 1), (128, 64, 1), (64, 64, 1), (64, 64, 1, 4), (128, 128, 3), (128, 64, 7), (64, 64, 2),
-         (64, 64, 3, 4)]
+         (64, 64, 3, 4),
+         # whole-K tiles beside split ones in one launch
+         (128, 128, 3, 1, 2), (128, 64, 7, 1, 1), (64, 64, 2, 1, 5), (64, 64, 3, 4, 7), (64, 64, 5, 1, 11)]
 TRANS = [(False, False), (False, True), (True, False), (True, True)]
 
 
@@ -108,6 +110,14 @@ def test_batched_auto_plan_split():
     run_case(96, 64, 512, False, False, "normal", "normal", batch=3, seed=52)
 
 
+@pytest.mark.parametrize("plan", [(64, 64, 3, 1, 3), (64, 64, 2, 4, 1), (128, 64, 4, 1, 4), (64, 64, 3, 1, 100),
+                                  (64, 64, 3, 1, 9)], ids=lambda p: "x".join(map(str, p)))
+def test_batched_whole_and_split_tiles(plan):
+    # Two tiles per matrix, ten in all: the split tiles start inside a
+    # matrix and run across the following ones; whole_tiles >= 10 splits none.
+    run_case(70, 40, 150, False, True, "normal", "zeros_tiny", batch=5, seed=53, plan=plan)
+
+
 def test_batched_broadcast_stride_zero():
     import torch
     note("bmm with a stride-0 (broadcast) B")
@@ -142,6 +152,33 @@ def test_k1_equals_elementwise():
     assert np.array_equal(c, want)
 
 
+@pytest.mark.parametrize("tile,kg,batch", [((64, 64), 1, 1), ((128, 64), 1, 2), ((64, 64), 4, 3)])
+def test_whole_and_split_tiles_match_their_plans(tile, kg, batch):
+    # Under a plan with whole-K tiles beside split ones, every whole tile is
+    # bit for bit the unsplit plan's and every split tile the split plan's
+    # (same K slices, added in the same order).
+    import torch
+    bm, bn = tile
+    m, n, k = 200, 130, 700
+    note(f"whole / split tiles vs their plans tile={tile} kgroups={kg} batch={batch}")
+    g = np.random.default_rng(74)
+    a = to_dev(g.standard_normal((batch, m, k)).astype(np.float32))
+    b = to_dev(g.standard_normal((batch, k, n)).astype(np.float32))
+    tiles_m, tiles_n = -(-m // bm), -(-n // bn)
+    total = batch * tiles_m * tiles_n
+    whole = total // 2 + 1
+    unsplit = pam.bmm(a, b, plan=(bm, bn, 1, kg))
+    split = pam.bmm(a, b, plan=(bm, bn, 4, kg))
+    mixed = pam.bmm(a, b, plan=(bm, bn, 4, kg, whole))
+    assert not torch.equal(unsplit.view(torch.int32), split.view(torch.int32))
+    for t in range(total):
+        z, r = divmod(t, tiles_m * tiles_n)
+        tm, tn = divmod(r, tiles_n)
+        sl = (z, slice(tm * bm, (tm + 1) * bm), slice(tn * bn, (tn + 1) * bn))
+        want = unsplit if t < whole else split
+        assert torch.equal(mixed[sl].view(torch.int32), want[sl].view(torch.int32)), f"tile {t}"
+
+
 def test_k0_writes_zeros():
     import torch
     note("gemm K = 0")
@@ -158,7 +195,7 @@ def test_deterministic():
     g = np.random.default_rng(73)
     a = to_dev(g.standard_normal((1, 200, 900)).astype(np.float32))
     b = to_dev(g.standard_normal((1, 900, 120)).astype(np.float32))
-    for plan in ((64, 64, 6), (64, 64, 3, 4)):
+    for plan in ((64, 64, 6), (64, 64, 3, 4), (64, 64, 3, 1, 2)):
         c1 = pam.bmm(a, b, plan=plan)
         c2 = pam.bmm(a, b, plan=plan)
         assert torch.equal(c1.view(torch.int32), c2.view(torch.int32))

@@ -87,19 +87,29 @@ def cpu_baseline(workload_id: int, host, forms, target_s: float) -> dict:
         pam_c.pam_gemm(a, b, form.trans_a, form.trans_b, form.m, form.n, form.k, form.lda, form.ldb, rows=rows)
         return time.perf_counter() - t0, count * form.n * form.k
 
-    # Probe with a small slice per product, then scale the slice to the target time.
-    per_form = target_s / len(forms)
-    total_t, total_macs, parts = 0.0, 0, []
-    for form in forms:
-        limit = form.batch if form.batch > 1 else form.m
-        count = min(limit, max(1, threads))
-        t, macs = run(form, count)
-        if t < per_form / 4:
-            count = min(limit, max(count, int(count * per_form / max(t, 1e-3))))
+    def sample(target, start):
+        # Probe with a small slice per product, then scale the slice to the target time.
+        per_form = target / len(forms)
+        total_t, total_macs, parts = 0.0, 0, []
+        for form in forms:
+            limit = form.batch if form.batch > 1 else form.m
+            count = min(limit, max(1, start))
             t, macs = run(form, count)
-        total_t += t
-        total_macs += macs
-        parts.append(f"{form.name}: {count} {'batch entries' if form.batch > 1 else 'rows'}")
+            if t < per_form / 4:
+                count = min(limit, max(count, int(count * per_form / max(t, 1e-3))))
+                t, macs = run(form, count)
+            total_t += t
+            total_macs += macs
+            parts.append(f"{form.name}: {count} {'batch entries' if form.batch > 1 else 'rows'}")
+        return total_macs, total_t, parts
+
+    total_macs, total_t, parts = sample(target_s, threads)
+    # The same oracle on one core, on a smaller sample.
+    pam_c.set_threads(1)
+    try:
+        one_macs, one_t, one_parts = sample(max(1.0, target_s / 8), 1)
+    finally:
+        pam_c.set_threads(threads)
     return {
         "value": total_macs / total_t / 1e9,
         "unit": "GPAM-MAC/s",
@@ -107,6 +117,8 @@ def cpu_baseline(workload_id: int, host, forms, target_s: float) -> dict:
         "kind": "oracle",
         "sample": f"workload {workload_id} ({'; '.join(parts)}), C oracle, float64 accumulate, "
                   f"{total_macs:.3e} PAM-MACs in {total_t:.1f} s",
+        "one_core": {"value": one_macs / one_t / 1e9, "unit": "GPAM-MAC/s",
+                     "sample": f"{'; '.join(one_parts)}, {one_macs:.3e} PAM-MACs in {one_t:.1f} s"},
     }
 
 

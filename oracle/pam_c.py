@@ -49,12 +49,19 @@ def load() -> ctypes.CDLL:
                                     ctypes.c_void_p, i64,
                                     ctypes.c_void_p, ctypes.c_void_p]
     lib.pam_oracle_num_threads.restype = ctypes.c_int
+    lib.pam_oracle_set_threads.restype = None
+    lib.pam_oracle_set_threads.argtypes = [ctypes.c_int]
     _lib = lib
     return lib
 
 
 def num_threads() -> int:
     return int(load().pam_oracle_num_threads())
+
+
+def set_threads(n: int) -> None:
+    """Thread count of the oracle's parallel loops from now on."""
+    load().pam_oracle_set_threads(int(n))
 
 
 def pam_mul(a: np.ndarray, b: np.ndarray) -> np.ndarray:

@@ -116,3 +116,10 @@ int pam_oracle_num_threads(void)
     return 1;
 #endif
 }
+
+/* Sets the thread count of the parallel loops that follow (n < 1 -> 1). */
+void pam_oracle_set_threads(int n)
+{
+    extern void omp_set_num_threads(int);
+    omp_set_num_threads(n > 0 ? n : 1);
+}

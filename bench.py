@@ -33,7 +33,8 @@ ALGO_LANE_OPS_PER_MAC = 2
 # float32-vector figure counted as one lane op per fma.
 NOMINAL_VALU_LANE_OPS = 256 * 4 * 32 * 2.4e9
 # The GEMM kernel's sources: a committed traffic summary is valid only for these bytes.
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2305_17190_amd", "csrc", f) for f in ("pam_kernels.hip", "pam_tile.h")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2305_17190_amd", "csrc", f)
+                  for f in ("pam_kernels.hip", "pam_tile.h", "pam_scalar.h")]
 
 
 def log(msg: str) -> None:
@@ -124,7 +125,7 @@ def cpu_baseline(workload_id: int, host, forms, target_s: float) -> dict:
 
 ELEMENTWISE_OPS = {
     # op: (binding name, kernel, bytes per element, input description)
-    "mul": ("mul", "pam_mul_vec4_kernel", 12, "N(0,1) with 1% zeros and 1% powers of two"),
+    "mul": ("mul", "binary_vec4_kernel<PamOp>", 12, "N(0,1) with 1% zeros and 1% powers of two"),
     "pad": ("pad", "binary_vec4_kernel<PadOp>", 12, "N(0,1) with 1% zeros and 1% powers of two"),
     "palog2": ("palog2", "unary_vec4_kernel<Palog2Op>", 8, "|N(0,1)| with 1% zeros and 1% powers of two"),
     "paexp2": ("paexp2", "unary_vec4_kernel<Paexp2Op>", 8, "softmax-shaped arguments"),

@@ -1,7 +1,11 @@
-// HIP kernels for the other elementwise piecewise affine operations on gfx950
-// (Kosson & Jaggi, Sec. 2.3): piecewise affine division (PAD), palog2 and
-// paexp2.  All three are HBM-bound streams; each element goes through a
-// branch-free integer / float sequence of a few full-rate vector ops.
+// HIP kernels for the elementwise piecewise affine operations on gfx950
+// (Kosson & Jaggi, Sec. 2.2-2.3): PAM itself, piecewise affine division (PAD),
+// palog2 and paexp2, and the mantissa rounding of the narrow products.  All
+// are HBM-bound streams; each element goes through a branch-free integer /
+// float sequence of a few vector ops.
+//
+// PAM is the complete per-element definition shared with the matrix products
+// (pam_scalar.h).
 //
 // PAD is the inverse of PAM: the int32 difference of the two encodings plus
 // one exponent bias (127 << 23); the borrow of the subtraction realises
@@ -28,18 +32,16 @@
 #include <algorithm>
 
 #include "pam_internal.h"
+#include "pam_scalar.h"
 
 namespace pamk {
 namespace {
 
-constexpr uint32_t kSign = 0x80000000u;
-constexpr uint32_t kMag = 0x7FFFFFFFu;
-constexpr uint32_t kBias = 0x3F800000u;
-constexpr uint32_t kMinNormal = 0x00800000u;
-constexpr uint32_t kFltMax = 0x7F7FFFFFu;
-constexpr uint32_t kInf = 0x7F800000u;
 constexpr uint32_t kNegInf = 0xFF800000u;
-constexpr uint32_t kQNaN = 0x7FC00000u;
+
+struct PamOp {
+    __device__ __forceinline__ uint32_t operator()(uint32_t ua, uint32_t ub) const { return pam_full(ua, ub); }
+};
 
 struct PadOp {
     __device__ __forceinline__ uint32_t operator()(uint32_t ua, uint32_t ub) const {
@@ -105,15 +107,22 @@ struct RoundOp {
     }
 };
 
+// 16-byte groups, read and written with non-temporal hints (a stream touches
+// each byte once), one group per thread: with a workgroup per 256 groups the
+// chip keeps far more loads in flight than a short grid-stride loop would.
+// The grid-stride loop only runs past kMaxBlocks workgroups.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 template <typename Op>
-__global__ void __launch_bounds__(256) binary_vec4_kernel(const uint4 *__restrict__ a, const uint4 *__restrict__ b,
-                                                          uint4 *__restrict__ out, int64_t n4) {
+__global__ void __launch_bounds__(256) binary_vec4_kernel(const u32x4 *__restrict__ a, const u32x4 *__restrict__ b,
+                                                          u32x4 *__restrict__ out, int64_t n4) {
     const Op op;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-        const uint4 x = a[i];
-        const uint4 y = b[i];
-        out[i] = make_uint4(op(x.x, y.x), op(x.y, y.y), op(x.z, y.z), op(x.w, y.w));
+        const u32x4 x = __builtin_nontemporal_load(a + i);
+        const u32x4 y = __builtin_nontemporal_load(b + i);
+        const u32x4 r = {op(x.x, y.x), op(x.y, y.y), op(x.z, y.z), op(x.w, y.w)};
+        __builtin_nontemporal_store(r, out + i);
     }
 }
 
@@ -124,16 +133,18 @@ __global__ void __launch_bounds__(256) binary_scalar_kernel(const uint32_t *__re
     const Op op;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-        out[i] = op(a[i], b[i]);
+        __builtin_nontemporal_store(op(__builtin_nontemporal_load(a + i), __builtin_nontemporal_load(b + i)),
+                                    out + i);
 }
 
 template <typename Op>
-__global__ void __launch_bounds__(256) unary_vec4_kernel(const uint4 *__restrict__ a, uint4 *__restrict__ out,
+__global__ void __launch_bounds__(256) unary_vec4_kernel(const u32x4 *__restrict__ a, u32x4 *__restrict__ out,
                                                          int64_t n4, Op op) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-        const uint4 x = a[i];
-        out[i] = make_uint4(op(x.x), op(x.y), op(x.z), op(x.w));
+        const u32x4 x = __builtin_nontemporal_load(a + i);
+        const u32x4 r = {op(x.x), op(x.y), op(x.z), op(x.w)};
+        __builtin_nontemporal_store(r, out + i);
     }
 }
 
@@ -142,13 +153,13 @@ __global__ void __launch_bounds__(256) unary_scalar_kernel(const uint32_t *__res
                                                            int64_t n, Op op) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-        out[i] = op(a[i]);
+        __builtin_nontemporal_store(op(__builtin_nontemporal_load(a + i)), out + i);
 }
 
-// Grid-stride launches: at most 16 workgroups of 256 threads per compute unit
-// (4096 on the chip); 16-byte groups when every pointer is 16-byte aligned,
-// then the scalar kernel for the remaining 0..3 elements (or everything).
-constexpr int64_t kMaxBlocks = 256 * 16;
+// Workgroups per launch at most (the grid, in threads, stays below 2^32);
+// 16-byte groups when every pointer is 16-byte aligned, then the scalar
+// kernel for the remaining 0..3 elements (or everything).
+constexpr int64_t kMaxBlocks = 16777215;
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -162,8 +173,8 @@ hipError_t launch_binary(const float *a, const float *b, float *out, int64_t n, 
         if (n4 > 0) {
             const int64_t blocks = std::min<int64_t>((n4 + 255) / 256, kMaxBlocks);
             hipLaunchKernelGGL(binary_vec4_kernel<Op>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                               reinterpret_cast<const uint4 *>(a), reinterpret_cast<const uint4 *>(b),
-                               reinterpret_cast<uint4 *>(out), n4);
+                               reinterpret_cast<const u32x4 *>(a), reinterpret_cast<const u32x4 *>(b),
+                               reinterpret_cast<u32x4 *>(out), n4);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess)
                 return e;
@@ -191,7 +202,7 @@ hipError_t launch_unary(const float *a, float *out, int64_t n, hipStream_t strea
         if (n4 > 0) {
             const int64_t blocks = std::min<int64_t>((n4 + 255) / 256, kMaxBlocks);
             hipLaunchKernelGGL(unary_vec4_kernel<Op>, dim3((unsigned)blocks), dim3(256), 0, stream,
-                               reinterpret_cast<const uint4 *>(a), reinterpret_cast<uint4 *>(out), n4, op);
+                               reinterpret_cast<const u32x4 *>(a), reinterpret_cast<u32x4 *>(out), n4, op);
             hipError_t e = hipGetLastError();
             if (e != hipSuccess)
                 return e;
@@ -210,6 +221,10 @@ hipError_t launch_unary(const float *a, float *out, int64_t n, hipStream_t strea
 }
 
 }  // namespace
+
+hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream) {
+    return launch_binary<PamOp>(a, b, out, n, stream);
+}
 
 hipError_t launch_pad(const float *a, const float *b, float *out, int64_t n, hipStream_t stream) {
     return launch_binary<PadOp>(a, b, out, n, stream);

@@ -1,4 +1,5 @@
-// HIP kernels for piecewise affine multiplication (PAM) on gfx950.
+// HIP kernels for piecewise affine multiplication (PAM) matrix products on
+// gfx950.
 //
 // PAM (Kosson & Jaggi, Sec. 2.2): the product of two float32 numbers is
 // replaced by the int32 sum of their encodings minus one exponent bias
@@ -60,92 +61,9 @@
 
 namespace pamk {
 
-enum : int { kScaled = 0, kSpecial = 1 };
-
-// Complete PAM of two float32 encodings, every input class.
-__device__ __forceinline__ uint32_t pam_full(uint32_t ua, uint32_t ub) {
-    const uint32_t s = (ua ^ ub) & kSign;
-    const uint32_t ma = ua & kMag;
-    const uint32_t mb = ub & kMag;
-    const uint32_t sum = ma + mb;                       // <= 0xFFFFFFFE, no wrap
-    uint32_t r = sum - kBias;
-    r = (sum < kBias + kMinNormal) ? 0u : r;            // underflow -> zero
-    r = (sum > kBias + kFltMax) ? kFltMax : r;          // overflow -> FLT_MAX
-    r = (ma < kMinNormal || mb < kMinNormal) ? 0u : r;  // zero / denormal operand
-    uint32_t out = s | r;
-    const bool a_inf = ma == kInf;
-    const bool b_inf = mb == kInf;
-    const bool nan_in = (ma > kInf) || (mb > kInf);
-    const bool inf_zero = (a_inf && mb < kMinNormal) || (b_inf && ma < kMinNormal);
-    out = (a_inf || b_inf) ? (s | kInf) : out;
-    out = (nan_in || inf_zero) ? kQNaN : out;
-    return out;
-}
-
-// ---------------------------------------------------------------------------
-// Elementwise PAM.  HBM-bound: 8 bytes read and 4 written per element.
-// ---------------------------------------------------------------------------
-
-__global__ void __launch_bounds__(256) pam_mul_vec4_kernel(const uint4 *__restrict__ a,
-                                                           const uint4 *__restrict__ b,
-                                                           uint4 *__restrict__ out, int64_t n4) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-        const uint4 x = a[i];
-        const uint4 y = b[i];
-        uint4 r;
-        r.x = pam_full(x.x, y.x);
-        r.y = pam_full(x.y, y.y);
-        r.z = pam_full(x.z, y.z);
-        r.w = pam_full(x.w, y.w);
-        out[i] = r;
-    }
-}
-
-__global__ void __launch_bounds__(256) pam_mul_scalar_kernel(const uint32_t *__restrict__ a,
-                                                             const uint32_t *__restrict__ b,
-                                                             uint32_t *__restrict__ out, int64_t n) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-        out[i] = pam_full(a[i], b[i]);
-}
-
-hipError_t launch_pam_mul(const float *a, const float *b, float *out, int64_t n, hipStream_t stream) {
-    if (n <= 0)
-        return hipSuccess;
-    const bool aligned = ((reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b) |
-                           reinterpret_cast<uintptr_t>(out)) & 15u) == 0;
-    const int64_t max_blocks = 256 * 16;
-    int64_t head = 0;
-    if (aligned) {
-        const int64_t n4 = n / 4;
-        if (n4 > 0) {
-            const int64_t blocks = std::min<int64_t>((n4 + 255) / 256, max_blocks);
-            hipLaunchKernelGGL(pam_mul_vec4_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                               reinterpret_cast<const uint4 *>(a), reinterpret_cast<const uint4 *>(b),
-                               reinterpret_cast<uint4 *>(out), n4);
-            hipError_t e = hipGetLastError();
-            if (e != hipSuccess)
-                return e;
-        }
-        head = n4 * 4;
-    }
-    const int64_t rest = n - head;
-    if (rest > 0) {
-        const int64_t blocks = std::min<int64_t>((rest + 255) / 256, max_blocks);
-        hipLaunchKernelGGL(pam_mul_scalar_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
-                           reinterpret_cast<const uint32_t *>(a) + head,
-                           reinterpret_cast<const uint32_t *>(b) + head,
-                           reinterpret_cast<uint32_t *>(out) + head, rest);
-        return hipGetLastError();
-    }
-    return hipSuccess;
-}
-
 // ---------------------------------------------------------------------------
 // Tiled PAM matrix product
 // ---------------------------------------------------------------------------
-
 
 // One micro-tile row, S1: acc[j] += a + b'[j] for j < 8.  When a and every
 // b[j] have exponent fields in [64, 190], the int32 sum of a's encoding and

@@ -1,5 +1,5 @@
-// Operand tile staging shared by the PAM matrix-product kernels: float32
-// encoding constants, the per-thread global-memory loader of a D x BK operand
+// Operand tile staging shared by the PAM matrix-product kernels: the
+// per-thread global-memory loader of a D x BK operand
 // tile (16-byte loads at fixed per-thread offsets, ragged edges, k tail), its
 // scans and the SCALED-encoding LDS store, and the 8-value LDS fragment read.
 // Included by the HIP sources only.
@@ -9,20 +9,9 @@
 #include <stdint.h>
 
 #include "pam_internal.h"
+#include "pam_scalar.h"
 
 namespace pamk {
-
-constexpr uint32_t kSign = 0x80000000u;
-constexpr uint32_t kMag = 0x7FFFFFFFu;
-constexpr uint32_t kBias = 0x3F800000u;     // 127 << 23
-constexpr uint32_t kMinNormal = 0x00800000u;
-constexpr uint32_t kFltMax = 0x7F7FFFFFu;
-constexpr uint32_t kInf = 0x7F800000u;
-constexpr uint32_t kQNaN = 0x7FC00000u;
-constexpr uint32_t kExpMask = 0x7F800000u;
-
-constexpr uint32_t kSignExp = 0xFF800000u;
-constexpr uint32_t kMant = 0x007FFFFFu;
 
 // An operand tile of D (rows of op(A), or columns of op(B)) x kChunkK, staged
 // through registers.  KCONTIG: element (o, kk) of chunk c sits at

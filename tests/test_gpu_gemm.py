@@ -152,6 +152,20 @@ def test_k1_equals_elementwise():
     assert np.array_equal(c, want)
 
 
+def test_batch_beyond_one_launch():
+    # 2^24 + 3 one-element products: more workgroups than one launch may hold
+    # (2^24 - 1), so the library issues two launches; every product is a K = 1
+    # sum, i.e. pam_mul of the two elements.
+    import pam_workloads as wl
+    n = (1 << 24) + 3
+    note(f"bmm batch={n} of 1x1x1 products (two launches)")
+    a, b = wl.pam_mul_inputs(n, 75)
+    c = pam.bmm(to_dev(a.reshape(n, 1, 1)), to_dev(b.reshape(n, 1, 1))).cpu().numpy().reshape(n)
+    want = pam_ref.pam_mul_ref(a, b)
+    bad = np.flatnonzero(c != want)
+    assert bad.size == 0, f"{bad.size} products differ, first at batch entry {bad[0]}"
+
+
 @pytest.mark.parametrize("tile,kg,batch", [((64, 64), 1, 1), ((128, 64), 1, 2), ((64, 64), 4, 3)])
 def test_whole_and_split_tiles_match_their_plans(tile, kg, batch):
     # Under a plan with whole-K tiles beside split ones, every whole tile is

@@ -203,7 +203,7 @@ pam_status_t validate(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
         return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
     if (sa < 0 || sb < 0 || sc < 0)
         return fail(PAM_ERROR_INVALID_VALUE, "batch strides must be >= 0");
-    if (lda > kMaxLd || ldb > kMaxLd)
+    if (lda >= kMaxLd || ldb >= kMaxLd)
         return fail(PAM_ERROR_NOT_SUPPORTED, "lda and ldb must be below 2^22 (per-thread 32-bit offsets)");
     const int64_t min_lda = std::max<int64_t>(1, ta == PAM_OP_N ? k : m);
     const int64_t min_ldb = std::max<int64_t>(1, tb == PAM_OP_N ? n : k);

@@ -132,9 +132,14 @@ def test_with_plan_rejects_bad_tiles(lib, plan):
 
 
 def test_leading_dimension_limit(lib):
-    big = 1 << 23
-    assert gemm_call(lib, lda=big) == 3
-    assert b"2^22" in lib.pam_last_error()
+    for big in (1 << 23, 1 << 22):
+        for kw in (dict(lda=big), dict(ldb=big)):
+            assert gemm_call(lib, **kw) == 3
+            assert b"2^22" in lib.pam_last_error()
+    # Just below the limit the arguments are valid (the call then fails only
+    # for want of a device here, with another message).
+    gemm_call(lib, lda=(1 << 22) - 4, ldb=(1 << 22) - 4)
+    assert b"2^22" not in lib.pam_last_error()
 
 
 def test_binding_refuses_cpu_tensors():

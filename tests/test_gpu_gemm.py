@@ -152,6 +152,46 @@ def test_k1_equals_elementwise():
     assert np.array_equal(c, want)
 
 
+@pytest.mark.parametrize("ta", [False, True], ids=["AN", "AT"])
+@pytest.mark.parametrize("plan", [None, (128, 128, 1)], ids=["auto", "128x128"])
+def test_leading_dimensions_near_the_limit(ta, plan):
+    # lda = ldb = 2^22 - 4, the largest multiple of 4 the library takes: in a
+    # 128-row panel the kernels' 32-bit per-thread byte offsets reach ~2.1 GB.
+    # m = 130 crosses a panel; only the first columns of each row are used.
+    ld = (1 << 22) - 4
+    m, n, k = 130, 3, 5
+    g = np.random.default_rng(81)
+    a_rows, a_cols = (k, m) if ta else (m, k)
+    a_buf = np.zeros((a_rows, ld), np.float32)
+    a_buf[:, :a_cols] = g.standard_normal((a_rows, a_cols))
+    b_buf = np.zeros((k, ld), np.float32)
+    b_buf[:, :n] = g.standard_normal((k, n))
+    note(f"gemm lda=ldb={ld} m={m} n={n} k={k} ta={ta} plan={plan}")
+    da = to_dev(a_buf)[:, :a_cols]
+    db = to_dev(b_buf)[:, :n]
+    if plan is None:
+        c = pam.gemm(da, db, trans_a=ta).cpu().numpy()
+    else:
+        c = pam.bmm(da.unsqueeze(0), db.unsqueeze(0), trans_a=ta, plan=plan).cpu().numpy()[0]
+    del da, db
+    c_ref, s_ref = oracle_gemm(a_buf, b_buf, ta, False, m, n, k, ld, ld)
+    check_gemm(c, c_ref[0], s_ref[0], k, f"lda=ldb={ld} ta={ta} plan={plan}")
+
+
+def test_long_k_many_slices():
+    # K ~ 1e6 (odd) on a 3 x 5 output: the plan splits K into many slices.
+    m, n, k = 3, 5, 1_000_003
+    g = np.random.default_rng(82)
+    a = g.standard_normal((m, k)).astype(np.float32)
+    b = g.standard_normal((k, n)).astype(np.float32)
+    tm, tn, splits, kg, whole = pam.plan(m, n, k)
+    note(f"gemm m={m} n={n} k={k} plan={(tm, tn, splits, kg, whole)}")
+    assert splits >= 16
+    c = pam.gemm(to_dev(a), to_dev(b)).cpu().numpy()
+    c_ref, s_ref = oracle_gemm(a, b, False, False, m, n, k, k, n)
+    check_gemm(c, c_ref[0], s_ref[0], k, "long K")
+
+
 def test_batch_beyond_one_launch():
     # 2^24 + 3 one-element products: more workgroups than one launch may hold
     # (2^24 - 1), so the library issues two launches; every product is a K = 1

@@ -49,6 +49,7 @@
 #ifndef PAM_H_
 #define PAM_H_
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -212,6 +213,47 @@ pam_status_t pam_gemm_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t 
                                  const float *A, int64_t lda, const float *B, int64_t ldb,
                                  const float *Mod, int64_t ldm, float *C, int64_t ldc,
                                  hipStream_t stream);
+
+/*
+ * Caller-provided split-K workspace.  The matrix products above split K for
+ * long-K / few-tile shapes and then take the partial sums' buffer from the
+ * stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`).  For
+ * callers with their own device allocator (e.g. torch's caching allocator),
+ * these entry points take the buffer instead and allocate nothing.
+ *
+ * pam_gemm_workspace_size: *bytes = the workspace bytes that pam_gemm,
+ * pam_gemm_batched and pam_gemm_narrow (and pam_gemm_batched_ws) need for
+ * these sizes with the library's plan; 0 when the plan does not split K.
+ * m, n, k, batch >= 0 and below 2^31; bytes non-NULL.
+ *
+ * pam_gemm_batched_ws: pam_gemm_narrow's product (mantissa_bits = 23:
+ * pam_gemm_batched's), arguments as there, with the partial sums in
+ * `workspace`: device memory of workspace_bytes bytes, 16-byte aligned, that
+ * nothing else reads or writes until this call's kernels on `stream` have
+ * finished (stream order: a later call on the same stream may reuse it).
+ * workspace_bytes >= pam_gemm_workspace_size's value, else
+ * PAM_ERROR_INVALID_VALUE before any launch; workspace may be NULL when that
+ * value is 0.  The caller owns the workspace; its contents afterwards are
+ * unspecified.
+ *
+ * pam_gemm_exact_grad_workspace_size / pam_gemm_exact_grad_ws: the same for
+ * pam_gemm_exact_grad.
+ */
+pam_status_t pam_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t batch, size_t *bytes);
+
+pam_status_t pam_gemm_batched_ws(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                                 const float *A, int64_t lda, int64_t strideA,
+                                 const float *B, int64_t ldb, int64_t strideB,
+                                 float *C, int64_t ldc, int64_t strideC,
+                                 int64_t batch, int32_t mantissa_bits,
+                                 void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+pam_status_t pam_gemm_exact_grad_workspace_size(int64_t m, int64_t n, int64_t k, size_t *bytes);
+
+pam_status_t pam_gemm_exact_grad_ws(pam_op_t transA, int64_t m, int64_t n, int64_t k,
+                                    const float *A, int64_t lda, const float *B, int64_t ldb,
+                                    const float *Mod, int64_t ldm, float *C, int64_t ldc,
+                                    void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Figures of `device` that set the vector-ALU roofline: compute units,

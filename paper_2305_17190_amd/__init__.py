@@ -15,7 +15,9 @@ device every call raises.
     exact_grad(A, B, Mod, trans_a, out=None)   exact-derivative product (Table 1)
 
 Matrix arguments are float32 HIP tensors whose last dimension is contiguous
-(row stride = leading dimension).  op(X) = X^T when trans_x is True.  The
+(row stride = leading dimension).  Products that split K take their
+workspace from torch's caching allocator (the library's ``*_ws`` entry
+points), so a call never waits for the GPU.  op(X) = X^T when trans_x is True.  The
 linear layer Y = X W^T is ``gemm(X, W, trans_b=True)``; its backward
 products (approximate derivative, Table 1 of the paper) are
 ``gemm(dY, W)`` and ``gemm(dY, X, trans_a=True)``.
@@ -56,7 +58,8 @@ _lib = None
 # Every symbol include/pam.h declares.
 EXPORTS = ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm", "pam_gemm_batched",
            "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_plan", "pam_gemm_batched_with_plan",
-           "pam_device_info", "pam_status_string", "pam_last_error")
+           "pam_gemm_workspace_size", "pam_gemm_batched_ws", "pam_gemm_exact_grad_workspace_size",
+           "pam_gemm_exact_grad_ws", "pam_device_info", "pam_status_string", "pam_last_error")
 
 
 def library_path() -> str:
@@ -85,9 +88,16 @@ def load() -> ctypes.CDLL:
                                                i64, ctypes.POINTER(_Plan), vp]
     lib.pam_gemm_plan.argtypes = [i64, i64, i64, i64, ctypes.POINTER(_Plan)]
     lib.pam_device_info.argtypes = [i32, ctypes.POINTER(_DeviceInfo)]
+    sz, psz = ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)
+    lib.pam_gemm_workspace_size.argtypes = [i64, i64, i64, i64, psz]
+    lib.pam_gemm_batched_ws.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i32,
+                                        vp, sz, vp]
+    lib.pam_gemm_exact_grad_workspace_size.argtypes = [i64, i64, i64, psz]
+    lib.pam_gemm_exact_grad_ws.argtypes = [i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, i64, vp, sz, vp]
     for name in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm",
                  "pam_gemm_batched", "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_batched_with_plan",
-                 "pam_gemm_plan", "pam_device_info"):
+                 "pam_gemm_plan", "pam_device_info", "pam_gemm_workspace_size", "pam_gemm_batched_ws",
+                 "pam_gemm_exact_grad_workspace_size", "pam_gemm_exact_grad_ws"):
         getattr(lib, name).restype = i32
     lib.pam_status_string.argtypes = [i32]
     lib.pam_status_string.restype = ctypes.c_char_p
@@ -111,6 +121,31 @@ def _torch():
 def _stream_handle(t) -> int:
     torch = _torch()
     return torch.cuda.current_stream(t.device).cuda_stream
+
+
+# Split-K workspace bytes per (kind, sizes), as the library reports them.
+_ws_bytes = {}
+
+
+def _workspace(kind: str, sizes: tuple, device):
+    """(pointer, bytes, tensor) of the split-K workspace a product needs, taken
+    from torch's caching allocator on the current stream (stream-ordered, so
+    it stays reserved until the product's kernels are done); (None, 0, None)
+    when the product does not split K."""
+    key = (kind,) + sizes
+    nbytes = _ws_bytes.get(key)
+    if nbytes is None:
+        out = ctypes.c_size_t()
+        fn = load().pam_gemm_workspace_size if kind == "gemm" else load().pam_gemm_exact_grad_workspace_size
+        _check(fn(*sizes, ctypes.byref(out)))
+        nbytes = int(out.value)
+        if len(_ws_bytes) >= 4096:
+            _ws_bytes.clear()
+        _ws_bytes[key] = nbytes
+    if nbytes == 0:
+        return None, 0, None
+    buf = _torch().empty(nbytes, dtype=_torch().uint8, device=device)
+    return buf.data_ptr(), nbytes, buf
 
 
 def _require(t, name: str, ndim: int):
@@ -209,12 +244,11 @@ def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, mantissa_
             raise ValueError(f"out must be {m}x{n}")
     ta = PAM_OP_T if trans_a else PAM_OP_N
     tb = PAM_OP_T if trans_b else PAM_OP_N
-    if mantissa_bits == 23:
-        _check(load().pam_gemm(ta, tb, m, n, k, A.data_ptr(), _ld(A), B.data_ptr(), _ld(B), out.data_ptr(), _ld(out),
-                               _stream_handle(A)))
-    else:
-        _check(load().pam_gemm_narrow(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
-                                      out.data_ptr(), _ld(out), 0, 1, int(mantissa_bits), _stream_handle(A)))
+    ws, ws_bytes, keep = _workspace("gemm", (m, n, k, 1), A.device)
+    _check(load().pam_gemm_batched_ws(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
+                                      out.data_ptr(), _ld(out), 0, 1, int(mantissa_bits), ws, ws_bytes,
+                                      _stream_handle(A)))
+    del keep
     return out
 
 
@@ -244,12 +278,12 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
     args = (ta, tb, m, n, k, A.data_ptr(), _ld(A), A.stride(0), B.data_ptr(), _ld(B), B.stride(0),
             out.data_ptr(), _ld(out), out.stride(0), batch)
     lib = load()
-    if mantissa_bits != 23:
-        if plan is not None:
-            raise ValueError("plan and mantissa_bits cannot be combined")
-        _check(lib.pam_gemm_narrow(*args, int(mantissa_bits), _stream_handle(A)))
-    elif plan is None:
-        _check(lib.pam_gemm_batched(*args, _stream_handle(A)))
+    if plan is None:
+        ws, ws_bytes, keep = _workspace("gemm", (m, n, k, batch), A.device)
+        _check(lib.pam_gemm_batched_ws(*args, int(mantissa_bits), ws, ws_bytes, _stream_handle(A)))
+        del keep
+    elif mantissa_bits != 23:
+        raise ValueError("plan and mantissa_bits cannot be combined")
     else:
         if not 3 <= len(plan) <= 5:
             raise ValueError("plan is (tile_m, tile_n, splits[, kgroups[, whole_tiles]])")
@@ -279,9 +313,11 @@ def exact_grad(A, B, Mod, trans_a: bool = False, out=None):
         _require(out, "out", 2)
         if tuple(out.shape) != (m, n):
             raise ValueError(f"out must be {m}x{n}")
-    _check(load().pam_gemm_exact_grad(PAM_OP_T if trans_a else PAM_OP_N, m, n, k, A.data_ptr(), _ld(A),
-                                      B.data_ptr(), _ld(B), Mod.data_ptr(), _ld(Mod), out.data_ptr(), _ld(out),
-                                      _stream_handle(A)))
+    ws, ws_bytes, keep = _workspace("exact", (m, n, k), A.device)
+    _check(load().pam_gemm_exact_grad_ws(PAM_OP_T if trans_a else PAM_OP_N, m, n, k, A.data_ptr(), _ld(A),
+                                         B.data_ptr(), _ld(B), Mod.data_ptr(), _ld(Mod), out.data_ptr(), _ld(out),
+                                         ws, ws_bytes, _stream_handle(A)))
+    del keep
     return out
 
 

@@ -250,11 +250,78 @@ pam_status_t check_device() {
     return PAM_SUCCESS;
 }
 
+// How a plan's work items are launched: whole-K tiles, then `splits` slices
+// of each split tile.  A plan with whole-K tiles beside split ones runs as
+// one launch; otherwise launches take as many whole matrices as fit.
+struct Layout {
+    int64_t tiles;        // per matrix
+    int64_t total;        // tiles of the whole batch
+    int64_t splits;       // K slices of a split tile (1: none)
+    int64_t whole_tiles;  // > 0: a hybrid plan
+    int64_t per_launch;   // matrices per launch
+    int64_t ws_tiles;     // split tiles the workspace holds at once
+    size_t ws_bytes;
+};
+
+pam_status_t layout_of(const Plan &plan, int64_t m, int64_t n, int64_t batch, Layout *out) {
+    Layout L{};
+    L.tiles = ceil_div(m, plan.tile_m) * ceil_div(n, plan.tile_n);
+    L.total = L.tiles * batch;
+    L.splits = plan.splits > 1 ? plan.splits : 1;
+    if (plan.whole_tiles >= L.total)
+        L.splits = 1;
+    L.whole_tiles = L.splits > 1 ? plan.whole_tiles : 0;
+    const bool hybrid = L.whole_tiles > 0;
+    if (L.tiles > kMaxDim || L.tiles * L.splits > pamk::kMaxLaunchItems ||
+        (hybrid && L.whole_tiles + (L.total - L.whole_tiles) * L.splits > pamk::kMaxLaunchItems))
+        return fail(PAM_ERROR_INVALID_VALUE, "too many workgroups for one launch (output too large for the plan)");
+    L.per_launch = hybrid ? batch : std::max<int64_t>(1, pamk::kMaxLaunchItems / (L.tiles * L.splits));
+    L.ws_tiles = hybrid ? L.total - L.whole_tiles : (L.splits > 1 ? std::min(batch, L.per_launch) * L.tiles : 0);
+    L.ws_bytes = (size_t)L.splits * (size_t)L.ws_tiles * (size_t)plan.tile_m * (size_t)plan.tile_n * sizeof(float);
+    if (L.ws_tiles == 0)
+        L.ws_bytes = 0;
+    *out = L;
+    return PAM_SUCCESS;
+}
+
+// A caller-provided workspace (pointer and size), or none: the library then
+// takes the split-K partial sums from the stream-ordered allocator.
+struct Workspace {
+    void *ptr;
+    size_t bytes;
+};
+
+pam_status_t check_workspace(const Workspace *ws, size_t need) {
+    if (ws == nullptr || need == 0)
+        return PAM_SUCCESS;
+    char buf[160];
+    if (ws->bytes < need) {
+        snprintf(buf, sizeof buf, "workspace of %zu bytes is smaller than the %zu this product needs", ws->bytes,
+                 need);
+        return fail(PAM_ERROR_INVALID_VALUE, buf);
+    }
+    if (ws->ptr == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "workspace is NULL");
+    if ((reinterpret_cast<uintptr_t>(ws->ptr) & 15u) != 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "workspace must be 16-byte aligned");
+    return PAM_SUCCESS;
+}
+
 pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                       int64_t sa, const float *B, int64_t ldb, int64_t sb, float *C, int64_t ldc, int64_t sc,
-                      int64_t batch, const Plan &plan, hipStream_t stream, int round_drop = 0) {
+                      int64_t batch, const Plan &plan, hipStream_t stream, int round_drop = 0,
+                      const Workspace *ext = nullptr) {
     if (m == 0 || n == 0 || batch == 0)
         return PAM_SUCCESS;
+    Layout L{};
+    if (k > 0) {
+        pam_status_t st = layout_of(plan, m, n, batch, &L);
+        if (st != PAM_SUCCESS)
+            return st;
+        st = check_workspace(ext, L.ws_bytes);
+        if (st != PAM_SUCCESS)
+            return st;
+    }
     pam_status_t st = check_device();
     if (st != PAM_SUCCESS)
         return st;
@@ -284,50 +351,35 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     p.vec_b = aligned16(B) && ldb % 4 == 0 && (batch == 1 || sb % 4 == 0);
     p.vec_c = aligned16(C) && ldc % 4 == 0 && (batch == 1 || sc % 4 == 0);
     p.round_drop = round_drop;
-
-    // Work items per launch: whole-K tiles, then `splits` slices of each
-    // split tile.  A plan with whole-K tiles beside split ones runs as one
-    // launch; otherwise launches take as many whole matrices as fit.
-    const int64_t tiles = ceil_div(m, plan.tile_m) * p.tiles_n;
-    const int64_t total = tiles * batch;
-    int64_t splits = plan.splits > 1 ? plan.splits : 1;
-    if (plan.whole_tiles >= total)
-        splits = 1;
-    const int64_t whole_tiles = splits > 1 ? plan.whole_tiles : 0;
-    const bool hybrid = whole_tiles > 0;
-    if (tiles > kMaxDim || tiles * splits > pamk::kMaxLaunchItems ||
-        (hybrid && whole_tiles + (total - whole_tiles) * splits > pamk::kMaxLaunchItems))
-        return fail(PAM_ERROR_INVALID_VALUE, "too many workgroups for one launch (output too large for the plan)");
-    const int64_t per_launch = hybrid ? batch : std::max<int64_t>(1, pamk::kMaxLaunchItems / (tiles * splits));
-    p.tiles = (int32_t)tiles;
-    p.splits = (int32_t)splits;
+    p.tiles = (int32_t)L.tiles;
+    p.splits = (int32_t)L.splits;
 
     float *ws = nullptr;
-    const int64_t ws_tiles = hybrid ? total - whole_tiles : (splits > 1 ? std::min(batch, per_launch) * tiles : 0);
-    if (ws_tiles > 0) {
-        const size_t bytes = (size_t)splits * (size_t)ws_tiles * (size_t)plan.tile_m * (size_t)plan.tile_n *
-                             sizeof(float);
-        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), bytes, stream);
+    const bool own = L.ws_bytes > 0 && ext == nullptr;
+    if (L.ws_bytes > 0 && !own)
+        ws = static_cast<float *>(ext->ptr);
+    if (own) {
+        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), L.ws_bytes, stream);
         if (e != hipSuccess || ws == nullptr) {
             g_last_error = std::string("hipMallocAsync of the split-K workspace: ") + hipGetErrorString(e);
             return PAM_ERROR_ALLOC;
         }
     }
     pam_status_t result = PAM_SUCCESS;
-    for (int64_t b0 = 0; b0 < batch && result == PAM_SUCCESS; b0 += per_launch) {
-        const int64_t nb = std::min(per_launch, batch - b0);
+    for (int64_t b0 = 0; b0 < batch && result == PAM_SUCCESS; b0 += L.per_launch) {
+        const int64_t nb = std::min(L.per_launch, batch - b0);
         p.A = A + b0 * sa;
         p.B = B + b0 * sb;
         p.C = C + b0 * sc;
         p.W = ws;
-        if (hybrid) {
-            p.whole = (int32_t)whole_tiles;
-            p.split_tiles = (int32_t)(total - whole_tiles);
-        } else if (splits > 1) {
+        if (L.whole_tiles > 0) {
+            p.whole = (int32_t)L.whole_tiles;
+            p.split_tiles = (int32_t)(L.total - L.whole_tiles);
+        } else if (L.splits > 1) {
             p.whole = 0;
-            p.split_tiles = (int32_t)(nb * tiles);
+            p.split_tiles = (int32_t)(nb * L.tiles);
         } else {
-            p.whole = (int32_t)(nb * tiles);
+            p.whole = (int32_t)(nb * L.tiles);
             p.split_tiles = 0;
         }
         hipError_t e = pamk::launch_pam_gemm(plan.tile_m, plan.tile_n, plan.kgroups, ta == PAM_OP_T, tb == PAM_OP_T, p,
@@ -342,7 +394,7 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
                 result = fail_hip(e, "split-K reduce launch");
         }
     }
-    if (ws) {
+    if (own) {
         hipError_t e = hipFreeAsync(ws, stream);
         if (e != hipSuccess && result == PAM_SUCCESS)
             result = fail_hip(e, "hipFreeAsync of the split-K workspace");
@@ -377,6 +429,96 @@ int query_simds_per_cu(int device) {
         &ctx);
     hsa_shut_down();
     return ctx.simds;
+}
+
+// Exact-derivative products: 128 x 128 tiles, two workgroups per compute
+// unit; K is split while the tiles would not fill two rounds and each slice
+// keeps >= 4 chunks.  Partial sums [split][m][n].
+int64_t exact_grad_splits(int64_t m, int64_t n, int64_t k) {
+    const int64_t tiles = ceil_div(m, 128) * ceil_div(n, 128);
+    int64_t splits = 1;
+    while (tiles * splits < 4 * kComputeUnits && splits < kMaxSplits && k / (splits * 2) >= 4 * pamk::kChunkK)
+        splits *= 2;
+    return splits;
+}
+
+size_t exact_grad_workspace(int64_t m, int64_t n, int64_t k, int64_t *splits_out, int64_t *per_out) {
+    const int64_t splits = exact_grad_splits(m, n, k);
+    const int64_t per = ceil_div(ceil_div(k, splits), pamk::kChunkK) * pamk::kChunkK;
+    const int64_t used = ceil_div(k, per);
+    *splits_out = used;
+    *per_out = per;
+    return used > 1 ? (size_t)used * (size_t)m * (size_t)n * sizeof(float) : 0;
+}
+
+pam_status_t run_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                            const float *B, int64_t ldb, const float *Mod, int64_t ldm, float *C, int64_t ldc,
+                            hipStream_t stream, const Workspace *ext) {
+    pam_status_t st = validate(transA, PAM_OP_N, m, n, k, A, lda, 0, B, ldb, 0, C, ldc, 0, 1);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (ldm < std::max<int64_t>(1, n))
+        return fail(PAM_ERROR_INVALID_VALUE, "ldm must be >= max(1, n)");
+    if (m == 0 || n == 0)
+        return PAM_SUCCESS;
+    if (Mod == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "Mod is NULL");
+    int64_t splits = 1, per = k;
+    const size_t need = k > 0 ? exact_grad_workspace(m, n, k, &splits, &per) : 0;
+    st = check_workspace(ext, need);
+    if (st != PAM_SUCCESS)
+        return st;
+    st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    if (k == 0) {
+        hipError_t e = pamk::launch_fill_zero(C, (int32_t)m, (int32_t)n, ldc, 0, 1, stream);
+        return e == hipSuccess ? PAM_SUCCESS : fail_hip(e, "fill kernel launch");
+    }
+    pamk::GemmParams p{};
+    p.A = A;
+    p.B = B;
+    p.Mod = Mod;
+    p.lda = lda;
+    p.ldb = ldb;
+    p.ldm = ldm;
+    p.ldc = ldc;
+    p.m = (int32_t)m;
+    p.n = (int32_t)n;
+    p.k = (int32_t)k;
+    p.k_per_split = (int32_t)per;
+    p.splits = (int32_t)splits;
+    p.tiles_n = (int32_t)ceil_div(n, 128);
+    p.vec_a = aligned16(A) && lda % 4 == 0;
+    p.vec_b = aligned16(B) && ldb % 4 == 0;
+    float *ws = nullptr;
+    const bool own = need > 0 && ext == nullptr;
+    if (need > 0 && !own)
+        ws = static_cast<float *>(ext->ptr);
+    if (own) {
+        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), need, stream);
+        if (e != hipSuccess || ws == nullptr) {
+            g_last_error = std::string("hipMallocAsync of the split-K workspace: ") + hipGetErrorString(e);
+            return PAM_ERROR_ALLOC;
+        }
+    }
+    p.C = C;
+    p.W = ws;
+    pam_status_t result = PAM_SUCCESS;
+    hipError_t e = pamk::launch_pam_exact_grad(transA == PAM_OP_T, p, stream);
+    if (e != hipSuccess)
+        result = fail_hip(e, "exact-derivative kernel launch");
+    else if (ws) {
+        e = pamk::launch_splitk_reduce(ws, C, (int32_t)m, (int32_t)n, ldc, 0, p.splits, 1, stream);
+        if (e != hipSuccess)
+            result = fail_hip(e, "split-K reduce launch");
+    }
+    if (own) {
+        e = hipFreeAsync(ws, stream);
+        if (e != hipSuccess && result == PAM_SUCCESS)
+            result = fail_hip(e, "hipFreeAsync of the split-K workspace");
+    }
+    return result;
 }
 
 }  // namespace
@@ -484,6 +626,41 @@ pam_status_t pam_gemm_narrow(pam_op_t transA, pam_op_t transB, int64_t m, int64_
                     choose_plan(m, n, k, batch), stream, 23 - mantissa_bits);
 }
 
+pam_status_t pam_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t batch, size_t *bytes) {
+    if (bytes == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "bytes is NULL");
+    *bytes = 0;
+    if (m < 0 || n < 0 || k < 0 || batch < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n, k and batch must be >= 0");
+    if (m > kMaxDim || n > kMaxDim || k > kMaxDim)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
+    if (m == 0 || n == 0 || k == 0 || batch == 0)
+        return PAM_SUCCESS;
+    Layout L;
+    const pam_status_t st = layout_of(choose_plan(m, n, k, batch), m, n, batch, &L);
+    if (st != PAM_SUCCESS)
+        return st;
+    *bytes = L.ws_bytes;
+    return PAM_SUCCESS;
+}
+
+pam_status_t pam_gemm_batched_ws(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                                 const float *A, int64_t lda, int64_t strideA, const float *B, int64_t ldb,
+                                 int64_t strideB, float *C, int64_t ldc, int64_t strideC, int64_t batch,
+                                 int32_t mantissa_bits, void *workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
+    if (mantissa_bits < 0 || mantissa_bits > 23)
+        return fail(PAM_ERROR_INVALID_VALUE, "mantissa_bits must be in [0, 23]");
+    pam_status_t st = validate(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (m == 0 || n == 0 || batch == 0)
+        return PAM_SUCCESS;
+    const Workspace ws{workspace, workspace_bytes};
+    return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch,
+                    choose_plan(m, n, k, batch), stream, 23 - mantissa_bits, &ws);
+}
+
 pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t mantissa_bits, hipStream_t stream) {
     if (mantissa_bits < 0 || mantissa_bits > 23)
         return fail(PAM_ERROR_INVALID_VALUE, "mantissa_bits must be in [0, 23]");
@@ -510,69 +687,29 @@ pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t m
 pam_status_t pam_gemm_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                                  const float *B, int64_t ldb, const float *Mod, int64_t ldm, float *C, int64_t ldc,
                                  hipStream_t stream) {
-    pam_status_t st = validate(transA, PAM_OP_N, m, n, k, A, lda, 0, B, ldb, 0, C, ldc, 0, 1);
-    if (st != PAM_SUCCESS)
-        return st;
-    if (ldm < std::max<int64_t>(1, n))
-        return fail(PAM_ERROR_INVALID_VALUE, "ldm must be >= max(1, n)");
-    if (m == 0 || n == 0)
+    return run_exact_grad(transA, m, n, k, A, lda, B, ldb, Mod, ldm, C, ldc, stream, nullptr);
+}
+
+pam_status_t pam_gemm_exact_grad_workspace_size(int64_t m, int64_t n, int64_t k, size_t *bytes) {
+    if (bytes == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "bytes is NULL");
+    *bytes = 0;
+    if (m < 0 || n < 0 || k < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be >= 0");
+    if (m > kMaxDim || n > kMaxDim || k > kMaxDim)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
+    if (m == 0 || n == 0 || k == 0)
         return PAM_SUCCESS;
-    if (Mod == nullptr)
-        return fail(PAM_ERROR_INVALID_VALUE, "Mod is NULL");
-    st = check_device();
-    if (st != PAM_SUCCESS)
-        return st;
-    if (k == 0) {
-        hipError_t e = pamk::launch_fill_zero(C, (int32_t)m, (int32_t)n, ldc, 0, 1, stream);
-        return e == hipSuccess ? PAM_SUCCESS : fail_hip(e, "fill kernel launch");
-    }
-    // 128 x 128 tiles, two workgroups per compute unit; split K while the
-    // tiles would not fill two rounds and each slice keeps >= 4 chunks.
-    const int64_t tiles = ceil_div(m, 128) * ceil_div(n, 128);
-    int64_t splits = 1;
-    while (tiles * splits < 4 * kComputeUnits && splits < kMaxSplits && k / (splits * 2) >= 4 * pamk::kChunkK)
-        splits *= 2;
-    pamk::GemmParams p{};
-    p.A = A;
-    p.B = B;
-    p.Mod = Mod;
-    p.lda = lda;
-    p.ldb = ldb;
-    p.ldm = ldm;
-    p.ldc = ldc;
-    p.m = (int32_t)m;
-    p.n = (int32_t)n;
-    p.k = (int32_t)k;
-    p.k_per_split = (int32_t)(ceil_div(ceil_div(k, splits), pamk::kChunkK) * pamk::kChunkK);
-    p.splits = (int32_t)ceil_div(k, p.k_per_split);
-    p.tiles_n = (int32_t)ceil_div(n, 128);
-    p.vec_a = aligned16(A) && lda % 4 == 0;
-    p.vec_b = aligned16(B) && ldb % 4 == 0;
-    float *ws = nullptr;
-    if (p.splits > 1) {
-        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), (size_t)p.splits * m * n * sizeof(float), stream);
-        if (e != hipSuccess || ws == nullptr) {
-            g_last_error = std::string("hipMallocAsync of the split-K workspace: ") + hipGetErrorString(e);
-            return PAM_ERROR_ALLOC;
-        }
-    }
-    p.C = C;
-    p.W = ws;
-    pam_status_t result = PAM_SUCCESS;
-    hipError_t e = pamk::launch_pam_exact_grad(transA == PAM_OP_T, p, stream);
-    if (e != hipSuccess)
-        result = fail_hip(e, "exact-derivative kernel launch");
-    else if (ws) {
-        e = pamk::launch_splitk_reduce(ws, C, (int32_t)m, (int32_t)n, ldc, 0, p.splits, 1, stream);
-        if (e != hipSuccess)
-            result = fail_hip(e, "split-K reduce launch");
-    }
-    if (ws) {
-        e = hipFreeAsync(ws, stream);
-        if (e != hipSuccess && result == PAM_SUCCESS)
-            result = fail_hip(e, "hipFreeAsync of the split-K workspace");
-    }
-    return result;
+    int64_t splits, per;
+    *bytes = exact_grad_workspace(m, n, k, &splits, &per);
+    return PAM_SUCCESS;
+}
+
+pam_status_t pam_gemm_exact_grad_ws(pam_op_t transA, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
+                                    const float *B, int64_t ldb, const float *Mod, int64_t ldm, float *C,
+                                    int64_t ldc, void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    const Workspace ws{workspace, workspace_bytes};
+    return run_exact_grad(transA, m, n, k, A, lda, B, ldb, Mod, ldm, C, ldc, stream, &ws);
 }
 
 pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_plan_t *plan) {

@@ -173,3 +173,55 @@ def test_exact_grad_rejects_bad_arguments(lib):
     assert lib.pam_gemm_exact_grad(0, 4, 4, 4, 8, 4, 8, 4, None, 4, 8, 4, None) == 1   # Mod NULL
     assert lib.pam_gemm_exact_grad(2, 4, 4, 4, 8, 4, 8, 4, 8, 4, 8, 4, None) == 1      # bad transA
     assert lib.pam_gemm_exact_grad(0, 0, 4, 4, None, 4, 8, 4, None, 4, None, 4, None) == 0   # m == 0
+
+
+def _ws_size(lib, m, n, k, batch=1):
+    out = ctypes.c_size_t(12345)
+    st = lib.pam_gemm_workspace_size(m, n, k, batch, ctypes.byref(out))
+    return st, out.value
+
+
+def test_workspace_size_follows_the_plan(lib):
+    # Zero when the plan keeps K whole, splits x split tiles x tile otherwise.
+    for m, n, k, b in ((16384, 4096, 4096, 1), (4096, 4096, 16384, 1), (768, 192, 12608, 1), (256, 64, 256, 256),
+                       (5, 7, 3, 1), (8192, 2048, 512, 1)):
+        tm, tn, s, kg, whole = pam.plan(m, n, k, b)
+        st, got = _ws_size(lib, m, n, k, b)
+        assert st == 0
+        tiles = -(-m // tm) * -(-n // tn) * b
+        split_tiles = 0 if s == 1 else (tiles - whole if whole else tiles)
+        assert got == s * split_tiles * tm * tn * 4, (m, n, k, b)
+    assert _ws_size(lib, 0, 5, 5) == (0, 0)
+    assert _ws_size(lib, 5, 5, 0) == (0, 0)
+    assert _ws_size(lib, -1, 5, 5)[0] == 1
+    assert lib.pam_gemm_workspace_size(4, 4, 4, 1, None) == 1
+    out = ctypes.c_size_t(7)
+    assert lib.pam_gemm_exact_grad_workspace_size(4096, 4096, 16384, ctypes.byref(out)) == 0 and out.value == 0
+    assert lib.pam_gemm_exact_grad_workspace_size(256, 256, 16384, ctypes.byref(out)) == 0
+    assert out.value > 0 and out.value % (256 * 256 * 4) == 0
+    assert lib.pam_gemm_exact_grad_workspace_size(4, 4, 4, None) == 1
+
+
+def _gemm_ws(lib, m, n, k, ws, ws_bytes, bits=23):
+    # Fake, never dereferenced device pointers: every case fails validation
+    # before any launch.
+    return lib.pam_gemm_batched_ws(0, 0, m, n, k, 256, k, 0, 256, n, 0, 256, n, 0, 1, bits, ws, ws_bytes, None)
+
+
+def test_workspace_entry_point_rejects_bad_workspaces(lib):
+    m, n, k = 768, 192, 12608                    # a split-K plan
+    st, need = _ws_size(lib, m, n, k)
+    assert st == 0 and need > 0
+    assert _gemm_ws(lib, m, n, k, 4096, need - 4) == 1
+    assert b"smaller" in lib.pam_last_error()
+    assert _gemm_ws(lib, m, n, k, None, need) == 1
+    assert b"NULL" in lib.pam_last_error()
+    assert _gemm_ws(lib, m, n, k, 4096 + 4, need) == 1
+    assert b"aligned" in lib.pam_last_error()
+    assert _gemm_ws(lib, m, n, k, 4096, need, bits=24) == 1
+    # exact-derivative product: a long-K, few-tile shape needs a workspace
+    out = ctypes.c_size_t()
+    assert lib.pam_gemm_exact_grad_workspace_size(256, 256, 16384, ctypes.byref(out)) == 0
+    assert lib.pam_gemm_exact_grad_ws(0, 256, 256, 16384, 256, 16384, 256, 256, 256, 256, 256, 256,
+                                      4096, out.value - 4, None) == 1
+    assert b"smaller" in lib.pam_last_error()

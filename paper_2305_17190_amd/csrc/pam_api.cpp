@@ -1,5 +1,6 @@
 // C ABI of the PAM library: argument validation, plan selection, workspace
-// handling and launches.  The arithmetic lives in pam_kernels.hip.
+// handling and launches.  The arithmetic lives in the HIP sources
+// (pam_kernels.hip, pa_ops.hip, pam_exact_grad.hip).
 
 #include <hip/hip_runtime.h>
 #include <hsa/hsa.h>
@@ -30,7 +31,6 @@ pam_status_t fail_hip(hipError_t e, const char *what) {
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 constexpr int64_t kMaxDim = 0x7FFFFFFF;
-constexpr int64_t kMaxGridZ = 65535;
 constexpr int64_t kMaxSplits = 64;
 // 128 rows of a panel, in bytes, must fit the kernels' 32-bit offsets.
 constexpr int64_t kMaxLd = (int64_t)1 << 22;
@@ -326,13 +326,8 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     if (st != PAM_SUCCESS)
         return st;
     if (k == 0) {
-        for (int64_t b0 = 0; b0 < batch; b0 += kMaxGridZ) {
-            const int64_t nb = std::min(kMaxGridZ, batch - b0);
-            hipError_t e = pamk::launch_fill_zero(C + b0 * sc, (int32_t)m, (int32_t)n, ldc, sc, nb, stream);
-            if (e != hipSuccess)
-                return fail_hip(e, "fill kernel launch");
-        }
-        return PAM_SUCCESS;
+        hipError_t e = pamk::launch_fill_zero(C, (int32_t)m, (int32_t)n, ldc, sc, batch, stream);
+        return e == hipSuccess ? PAM_SUCCESS : fail_hip(e, "fill kernel launch");
     }
 
     pamk::GemmParams p{};

@@ -241,6 +241,13 @@ def test_k0_writes_zeros():
     c = torch.full((7, 9), 5.0, device=device())
     pam.gemm(a, b, out=c)
     assert torch.all(c == 0)
+    # batched, into a padded output: every product zero, the padding untouched
+    a3 = torch.empty((4, 5, 0), device=device())
+    b3 = torch.empty((4, 0, 6), device=device())
+    c3_full = torch.full((4, 5, 8), float("nan"), device=device())
+    pam.bmm(a3, b3, out=c3_full[:, :, :6])
+    assert torch.all(c3_full[:, :, :6] == 0)
+    assert torch.all(torch.isnan(c3_full[:, :, 6:]))
 
 
 def test_deterministic():

@@ -33,8 +33,8 @@ in the HIP library):
   R4  underflow (result exponent field <= 0) gives a signed zero; clamping the
       exponent field to 0 leaves a denormal encoding, which is flushed.
   R5  overflow (result exponent field >= 255) saturates to +-FLT_MAX, the
-      largest finite value ("clamping to the max value"), which keeps
-      |A .^ B| <= |A * B| for all finite operands.
+      largest finite value (the paper clamps overflowing results to the
+      maximum), which keeps |A .^ B| <= |A * B| for all finite operands.
   R6  NaN operand -> NaN; inf times zero/denormal -> NaN; inf times anything
       else -> signed inf.  NaN results are the canonical quiet NaN 0x7FC00000.
   R7  the bias removed is 127 << 23 = 0x3F800000, once, from the magnitude

@@ -1,0 +1,66 @@
+"""Seeded randomized parity sweep of the PAM matrix product against the C
+oracle: random sizes (ragged in every dimension), transposes, batch counts,
+padded leading dimensions and batch strides, every tile shape, random split
+counts and whole-tile counts (hybrid plans), plus the library's own plan.
+Each case is compared element by element within the GEMM tolerance."""
+import numpy as np
+import pytest
+
+import paper_2305_17190_amd as pam
+from gpu_util import check_gemm, device, note, oracle_gemm, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TILES = [(128, 128, 1), (128, 64, 1), (64, 64, 1), (64, 64, 4)]
+CASES = 120
+
+
+def draw(rng):
+    m = int(rng.integers(1, 300))
+    n = int(rng.integers(1, 300))
+    k = int(rng.integers(1, 700))
+    batch = int(rng.integers(1, 4))
+    while m * n * k * batch > 6_000_000:
+        k = max(1, k // 2)
+    ta, tb = bool(rng.integers(0, 2)), bool(rng.integers(0, 2))
+    pad = tuple(int(x) for x in rng.integers(0, 6, size=3))
+    choice = int(rng.integers(0, 6))
+    if choice == 0:
+        plan = None                                        # the library's plan
+    else:
+        tm, tn, kg = TILES[int(rng.integers(0, len(TILES)))]
+        splits = int(rng.integers(1, 9))
+        tiles = -(-m // tm) * -(-n // tn) * batch
+        whole = int(rng.integers(0, tiles + 1)) if choice >= 4 else 0
+        plan = (tm, tn, splits, kg, whole)
+    return m, n, k, batch, ta, tb, pad, plan
+
+
+@pytest.mark.parametrize("case", range(CASES))
+def test_random_products(case):
+    import torch
+    rng = np.random.default_rng(1000 + case)
+    m, n, k, batch, ta, tb, pad, plan = draw(rng)
+    a_rows, a_cols = (k, m) if ta else (m, k)
+    b_rows, b_cols = (n, k) if tb else (k, n)
+    lda, ldb, ldc = a_cols + pad[0], b_cols + pad[1], n + pad[2]
+    # batch strides: whole padded matrices, plus a few spare rows
+    sa, sb = (a_rows + 1) * lda, (b_rows + 2) * ldb
+    a_buf = rng.standard_normal(batch * sa).astype(np.float32)
+    b_buf = rng.standard_normal(batch * sb).astype(np.float32)
+    if case % 3 == 0:                                      # zeros, denormals and tiny values
+        for buf in (a_buf, b_buf):
+            idx = rng.choice(buf.size, size=max(1, buf.size // 50), replace=False)
+            buf[idx[0::3]] = 0.0
+            buf[idx[1::3]] = np.float32(3e-41)
+            buf[idx[2::3]] = np.float32(1.5e-38)
+    note(f"fuzz {case}: m={m} n={n} k={k} batch={batch} ta={ta} tb={tb} pad={pad} plan={plan}")
+    da = torch.as_strided(to_dev(a_buf), (batch, a_rows, a_cols), (sa, lda, 1))
+    db = torch.as_strided(to_dev(b_buf), (batch, b_rows, b_cols), (sb, ldb, 1))
+    c_full = torch.full((batch, m, ldc), float("nan"), device=device())
+    c = c_full[:, :, :n]
+    pam.bmm(da, db, trans_a=ta, trans_b=tb, out=c, plan=plan)
+    got = c_full.cpu().numpy()
+    assert np.all(np.isnan(got[:, :, n:])), "wrote outside the output's columns"
+    c_ref, s_ref = oracle_gemm(a_buf, b_buf, ta, tb, m, n, k, lda, ldb, sa, sb, batches=list(range(batch)))
+    check_gemm(got[:, :, :n], c_ref, s_ref, k, f"fuzz {case}")

@@ -266,13 +266,15 @@ struct Layout {
 pam_status_t layout_of(const Plan &plan, int64_t m, int64_t n, int64_t batch, Layout *out) {
     Layout L{};
     L.tiles = ceil_div(m, plan.tile_m) * ceil_div(n, plan.tile_n);
+    if (L.tiles > kMaxDim || batch > kMaxDim * kMaxDim / L.tiles)
+        return fail(PAM_ERROR_INVALID_VALUE, "too many output tiles (m, n or batch too large)");
     L.total = L.tiles * batch;
     L.splits = plan.splits > 1 ? plan.splits : 1;
     if (plan.whole_tiles >= L.total)
         L.splits = 1;
     L.whole_tiles = L.splits > 1 ? plan.whole_tiles : 0;
     const bool hybrid = L.whole_tiles > 0;
-    if (L.tiles > kMaxDim || L.tiles * L.splits > pamk::kMaxLaunchItems ||
+    if (L.tiles * L.splits > pamk::kMaxLaunchItems ||
         (hybrid && L.whole_tiles + (L.total - L.whole_tiles) * L.splits > pamk::kMaxLaunchItems))
         return fail(PAM_ERROR_INVALID_VALUE, "too many workgroups for one launch (output too large for the plan)");
     L.per_launch = hybrid ? batch : std::max<int64_t>(1, pamk::kMaxLaunchItems / (L.tiles * L.splits));

@@ -225,3 +225,10 @@ def test_workspace_entry_point_rejects_bad_workspaces(lib):
     assert lib.pam_gemm_exact_grad_ws(0, 256, 256, 16384, 256, 16384, 256, 256, 256, 256, 256, 256,
                                       4096, out.value - 4, None) == 1
     assert b"smaller" in lib.pam_last_error()
+
+
+def test_absurd_batch_is_refused_not_overflowed(lib):
+    # tiles x batch beyond 2^62: refused with a message, before any device call
+    st, _ = _ws_size(lib, 1 << 30, 1 << 30, 64, 1 << 40)
+    assert st == 1 and b"too many" in lib.pam_last_error()
+    assert lib.pam_gemm_batched(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1 << 62, None) == 1

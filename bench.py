@@ -257,6 +257,9 @@ def main() -> int:
                     help="time only one elementwise op on N elements (HBM roofline) and print its line")
     ap.add_argument("--mantissa-bits", type=int, default=23,
                     help="round every operand to this many mantissa bits first (narrow products; default 23 = none)")
+    ap.add_argument("--bf16", action="store_true",
+                    help="the workload's operands stored as bfloat16 (rounded once, before timing), products of "
+                         "the bfloat16 operands with float32 results")
     ap.add_argument("--autograd", action="store_true",
                     help="time one PAM linear layer forward + backward through autograd (w2, w5)")
     ap.add_argument("--exact-grad", action="store_true",
@@ -300,6 +303,8 @@ def main() -> int:
     log(f"generating workload {wid} ({spec['desc']})")
     host = wl.workload_inputs(wid)
     dt = {k: torch.from_numpy(v).to(dev) for k, v in host.items()}
+    if args.bf16:
+        dt = {k: v.to(torch.bfloat16) for k, v in dt.items()}
     outs = {}
     for f in forms:
         shape = (f.batch, f.m, f.n) if f.batch > 1 else (f.m, f.n)
@@ -371,6 +376,7 @@ def main() -> int:
             "pam_macs_per_step": macs_per_step,
             "parallelism": "single GPU",
             **({"mantissa_bits": args.mantissa_bits} if args.mantissa_bits != 23 else {}),
+            **({"operands": "bfloat16"} if args.bf16 else {}),
         },
         "roofline": {
             "bound": "alu",

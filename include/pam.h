@@ -248,6 +248,23 @@ pam_status_t pam_gemm_batched_ws(pam_op_t transA, pam_op_t transB, int64_t m, in
                                  int64_t batch, int32_t mantissa_bits,
                                  void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * bfloat16 operands (App. "PAM with Narrower Mantissas"; storage of 7-bit
+ * mantissa operands in half the bytes): A and B hold bfloat16 values (the
+ * high 16 bits of float32 encodings), leading dimensions and batch strides
+ * in elements.  Each element is widened exactly to float32 as it is loaded;
+ * the product is then pam_gemm_batched's on the widened operands, bit for bit
+ * (same plan), with float32 C.  Requirements as pam_gemm_batched.  workspace
+ * NULL: split-K partial sums from the stream-ordered allocator, as
+ * pam_gemm_batched; otherwise as pam_gemm_batched_ws (workspace_bytes >=
+ * pam_gemm_workspace_size's value).
+ */
+pam_status_t pam_gemm_batched_bf16(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                                   const uint16_t *A, int64_t lda, int64_t strideA,
+                                   const uint16_t *B, int64_t ldb, int64_t strideB,
+                                   float *C, int64_t ldc, int64_t strideC, int64_t batch,
+                                   void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 pam_status_t pam_gemm_exact_grad_workspace_size(int64_t m, int64_t n, int64_t k, size_t *bytes);
 
 pam_status_t pam_gemm_exact_grad_ws(pam_op_t transA, int64_t m, int64_t n, int64_t k,

@@ -10,7 +10,7 @@ device every call raises.
     pad(a, b, out=None)                        elementwise a ./ b (Sec. 2.3)
     palog2(a, out=None), paexp2(a, out=None)   elementwise (Sec. 2.3)
     round_mantissa(a, bits, out=None)          a rounded to `bits` mantissa bits
-    gemm(A, B, trans_a, trans_b, out=None)     C = op(A) .^ op(B)
+    gemm(A, B, trans_a, trans_b, out=None)     C = op(A) .^ op(B) (float32 or bfloat16 A, B)
     bmm(A, B, trans_a, trans_b, out=None)      batched over the leading axis
     exact_grad(A, B, Mod, trans_a, out=None)   exact-derivative product (Table 1)
 
@@ -58,7 +58,7 @@ _lib = None
 # Every symbol include/pam.h declares.
 EXPORTS = ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm", "pam_gemm_batched",
            "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_plan", "pam_gemm_batched_with_plan",
-           "pam_gemm_workspace_size", "pam_gemm_batched_ws", "pam_gemm_exact_grad_workspace_size",
+           "pam_gemm_workspace_size", "pam_gemm_batched_ws", "pam_gemm_batched_bf16", "pam_gemm_exact_grad_workspace_size",
            "pam_gemm_exact_grad_ws", "pam_device_info", "pam_status_string", "pam_last_error")
 
 
@@ -92,11 +92,14 @@ def load() -> ctypes.CDLL:
     lib.pam_gemm_workspace_size.argtypes = [i64, i64, i64, i64, psz]
     lib.pam_gemm_batched_ws.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i32,
                                         vp, sz, vp]
+    lib.pam_gemm_batched_bf16.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64,
+                                          vp, sz, vp]
     lib.pam_gemm_exact_grad_workspace_size.argtypes = [i64, i64, i64, psz]
     lib.pam_gemm_exact_grad_ws.argtypes = [i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, i64, vp, sz, vp]
     for name in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm",
                  "pam_gemm_batched", "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_batched_with_plan",
                  "pam_gemm_plan", "pam_device_info", "pam_gemm_workspace_size", "pam_gemm_batched_ws",
+                 "pam_gemm_batched_bf16",
                  "pam_gemm_exact_grad_workspace_size", "pam_gemm_exact_grad_ws"):
         getattr(lib, name).restype = i32
     lib.pam_status_string.argtypes = [i32]
@@ -148,12 +151,12 @@ def _workspace(kind: str, sizes: tuple, device):
     return buf.data_ptr(), nbytes, buf
 
 
-def _require(t, name: str, ndim: int):
+def _require(t, name: str, ndim: int, bf16_ok: bool = False):
     torch = _torch()
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
-    if t.dtype != torch.float32:
-        raise TypeError(f"{name} must be float32, got {t.dtype}")
+    if t.dtype != torch.float32 and not (bf16_ok and t.dtype == torch.bfloat16):
+        raise TypeError(f"{name} must be float32{' or bfloat16' if bf16_ok else ''}, got {t.dtype}")
     if not t.is_cuda:
         raise PamError(f"{name} must be a HIP (cuda) tensor; the PAM library has no CPU path")
     if t.dim() != ndim:
@@ -215,6 +218,18 @@ def round_mantissa(a, bits: int, out=None):
     return out
 
 
+def _bf16_pair(A, B, mantissa_bits) -> bool:
+    """True for two bfloat16 operands (their values already have 7 mantissa
+    bits); mixed float32 / bfloat16 operands are refused."""
+    torch = _torch()
+    a16, b16 = A.dtype == torch.bfloat16, B.dtype == torch.bfloat16
+    if a16 != b16:
+        raise TypeError("A and B must both be float32 or both bfloat16")
+    if a16 and int(mantissa_bits) < 7:
+        raise ValueError("bfloat16 operands have 7 mantissa bits; round float32 operands for fewer")
+    return a16
+
+
 def _dims(A, B, trans_a: bool, trans_b: bool):
     m, k = (A.shape[-1], A.shape[-2]) if trans_a else (A.shape[-2], A.shape[-1])
     kb, n = (B.shape[-1], B.shape[-2]) if trans_b else (B.shape[-2], B.shape[-1])
@@ -231,10 +246,13 @@ def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, mantissa_
     """C = op(A) .^ op(B) with float32 accumulation; returns C (m x n).
 
     ``mantissa_bits`` < 23 rounds every operand element to that many mantissa
-    bits first (App. "PAM with Narrower Mantissas")."""
+    bits first (App. "PAM with Narrower Mantissas").  A and B may both be
+    bfloat16 (7-bit mantissas in half the bytes): the kernels widen them
+    exactly to float32 as they load them; C is float32."""
     torch = _torch()
-    _require(A, "A", 2)
-    _require(B, "B", 2)
+    _require(A, "A", 2, bf16_ok=True)
+    _require(B, "B", 2, bf16_ok=True)
+    bf16 = _bf16_pair(A, B, mantissa_bits)
     m, n, k = _dims(A, B, trans_a, trans_b)
     if out is None:
         out = torch.empty((m, n), dtype=torch.float32, device=A.device)
@@ -245,9 +263,14 @@ def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, mantissa_
     ta = PAM_OP_T if trans_a else PAM_OP_N
     tb = PAM_OP_T if trans_b else PAM_OP_N
     ws, ws_bytes, keep = _workspace("gemm", (m, n, k, 1), A.device)
-    _check(load().pam_gemm_batched_ws(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
-                                      out.data_ptr(), _ld(out), 0, 1, int(mantissa_bits), ws, ws_bytes,
-                                      _stream_handle(A)))
+    lib = load()
+    if bf16:
+        _check(lib.pam_gemm_batched_bf16(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
+                                         out.data_ptr(), _ld(out), 0, 1, ws, ws_bytes, _stream_handle(A)))
+    else:
+        _check(lib.pam_gemm_batched_ws(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
+                                       out.data_ptr(), _ld(out), 0, 1, int(mantissa_bits), ws, ws_bytes,
+                                       _stream_handle(A)))
     del keep
     return out
 
@@ -261,8 +284,9 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
     many mantissa bits first (the library then picks the plan).
     """
     torch = _torch()
-    _require(A, "A", 3)
-    _require(B, "B", 3)
+    _require(A, "A", 3, bf16_ok=True)
+    _require(B, "B", 3, bf16_ok=True)
+    bf16 = _bf16_pair(A, B, mantissa_bits)
     if A.shape[0] != B.shape[0]:
         raise ValueError("batch sizes differ")
     batch = A.shape[0]
@@ -278,7 +302,13 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
     args = (ta, tb, m, n, k, A.data_ptr(), _ld(A), A.stride(0), B.data_ptr(), _ld(B), B.stride(0),
             out.data_ptr(), _ld(out), out.stride(0), batch)
     lib = load()
-    if plan is None:
+    if bf16:
+        if plan is not None:
+            raise ValueError("bfloat16 operands take the library's plan")
+        ws, ws_bytes, keep = _workspace("gemm", (m, n, k, batch), A.device)
+        _check(lib.pam_gemm_batched_bf16(*args, ws, ws_bytes, _stream_handle(A)))
+        del keep
+    elif plan is None:
         ws, ws_bytes, keep = _workspace("gemm", (m, n, k, batch), A.device)
         _check(lib.pam_gemm_batched_ws(*args, int(mantissa_bits), ws, ws_bytes, _stream_handle(A)))
         del keep

@@ -29,6 +29,7 @@ pam_status_t fail_hip(hipError_t e, const char *what) {
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned8(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
 constexpr int64_t kMaxDim = 0x7FFFFFFF;
 constexpr int64_t kMaxSplits = 64;
@@ -312,7 +313,7 @@ pam_status_t check_workspace(const Workspace *ws, size_t need) {
 pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                       int64_t sa, const float *B, int64_t ldb, int64_t sb, float *C, int64_t ldc, int64_t sc,
                       int64_t batch, const Plan &plan, hipStream_t stream, int round_drop = 0,
-                      const Workspace *ext = nullptr) {
+                      const Workspace *ext = nullptr, bool bf16 = false) {
     if (m == 0 || n == 0 || batch == 0)
         return PAM_SUCCESS;
     Layout L{};
@@ -344,8 +345,11 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     p.k = (int32_t)k;
     p.k_per_split = (int32_t)std::min<int64_t>(plan.k_per_split, kMaxDim);
     p.tiles_n = (int32_t)ceil_div(n, plan.tile_n);
-    p.vec_a = aligned16(A) && lda % 4 == 0 && (batch == 1 || sa % 4 == 0);
-    p.vec_b = aligned16(B) && ldb % 4 == 0 && (batch == 1 || sb % 4 == 0);
+    // Operand groups of four elements: 16 bytes (float32) or 8 (bfloat16).
+    const bool a_ok = bf16 ? aligned8(A) : aligned16(A);
+    const bool b_ok = bf16 ? aligned8(B) : aligned16(B);
+    p.vec_a = a_ok && lda % 4 == 0 && (batch == 1 || sa % 4 == 0);
+    p.vec_b = b_ok && ldb % 4 == 0 && (batch == 1 || sb % 4 == 0);
     p.vec_c = aligned16(C) && ldc % 4 == 0 && (batch == 1 || sc % 4 == 0);
     p.round_drop = round_drop;
     p.tiles = (int32_t)L.tiles;
@@ -365,8 +369,9 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     pam_status_t result = PAM_SUCCESS;
     for (int64_t b0 = 0; b0 < batch && result == PAM_SUCCESS; b0 += L.per_launch) {
         const int64_t nb = std::min(L.per_launch, batch - b0);
-        p.A = A + b0 * sa;
-        p.B = B + b0 * sb;
+        const size_t es = bf16 ? 2 : 4;   // operand element bytes
+        p.A = reinterpret_cast<const float *>(reinterpret_cast<const char *>(A) + (size_t)(b0 * sa) * es);
+        p.B = reinterpret_cast<const float *>(reinterpret_cast<const char *>(B) + (size_t)(b0 * sb) * es);
         p.C = C + b0 * sc;
         p.W = ws;
         if (L.whole_tiles > 0) {
@@ -379,8 +384,8 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
             p.whole = (int32_t)(nb * L.tiles);
             p.split_tiles = 0;
         }
-        hipError_t e = pamk::launch_pam_gemm(plan.tile_m, plan.tile_n, plan.kgroups, ta == PAM_OP_T, tb == PAM_OP_T, p,
-                                             stream);
+        hipError_t e = pamk::launch_pam_gemm(plan.tile_m, plan.tile_n, plan.kgroups, ta == PAM_OP_T, tb == PAM_OP_T,
+                                             bf16, p, stream);
         if (e != hipSuccess) {
             result = fail_hip(e, "gemm kernel launch");
             break;
@@ -656,6 +661,22 @@ pam_status_t pam_gemm_batched_ws(pam_op_t transA, pam_op_t transB, int64_t m, in
     const Workspace ws{workspace, workspace_bytes};
     return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch,
                     choose_plan(m, n, k, batch), stream, 23 - mantissa_bits, &ws);
+}
+
+pam_status_t pam_gemm_batched_bf16(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                                   const uint16_t *A, int64_t lda, int64_t strideA, const uint16_t *B, int64_t ldb,
+                                   int64_t strideB, float *C, int64_t ldc, int64_t strideC, int64_t batch,
+                                   void *workspace, size_t workspace_bytes, hipStream_t stream) {
+    const float *a = reinterpret_cast<const float *>(A);
+    const float *b = reinterpret_cast<const float *>(B);
+    pam_status_t st = validate(transA, transB, m, n, k, a, lda, strideA, b, ldb, strideB, C, ldc, strideC, batch);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (m == 0 || n == 0 || batch == 0)
+        return PAM_SUCCESS;
+    const Workspace ws{workspace, workspace_bytes};
+    return run_gemm(transA, transB, m, n, k, a, lda, strideA, b, ldb, strideB, C, ldc, strideC, batch,
+                    choose_plan(m, n, k, batch), stream, 0, workspace != nullptr ? &ws : nullptr, true);
 }
 
 pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t mantissa_bits, hipStream_t stream) {

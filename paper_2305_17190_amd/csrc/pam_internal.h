@@ -19,7 +19,7 @@ constexpr int kChunkK = 16;
 // [s * k_per_split, (s + 1) * k_per_split)) of tile whole + t into the
 // tile-packed partial sums W[s][t][tile_m][tile_n].
 struct GemmParams {
-    const float *A;
+    const float *A;    // operands (bfloat16 elements for the bfloat16 products)
     const float *B;
     float *C;          // final output
     float *W;          // partial sums of the split tiles, or nullptr (layout per kernel)
@@ -53,7 +53,9 @@ hipError_t launch_round_mantissa(const float *a, float *out, int64_t n, int drop
 
 // (tile_m, tile_n, kgroups) in {(128,128,1), (128,64,1), (64,64,1), (64,64,4)};
 // a one-dimensional grid of p.whole + p.split_tiles * p.splits workgroups.
-hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b,
+// bf16: p.A and p.B hold bfloat16 elements (leading dimensions and strides
+// in elements), widened exactly to float32 as they are loaded.
+hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, bool bf16,
                            const GemmParams &p, hipStream_t stream);
 
 // C of the split tiles of a matrix product launch: element by element the sum

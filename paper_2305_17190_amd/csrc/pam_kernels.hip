@@ -171,7 +171,7 @@ constexpr int gemm_waves_per_simd(int bm, int bn, int kw) { return (bm == 128 &&
 // and takes 16 of the 16 * KW k steps of every LDS chunk; with KW > 1 the
 // groups' partial tiles are added through LDS at the end, so small outputs
 // get more waves without extra HBM traffic.
-template <int BM, int BN, int KW, bool TA, bool TB>
+template <int BM, int BN, int KW, bool TA, bool TB, typename T>
 __global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(gemm_waves_per_simd(BM, BN, KW))))
 pam_gemm_kernel(GemmParams p) {
     constexpr int KPG = kChunkK;           // k steps per group per chunk
@@ -226,15 +226,17 @@ pam_gemm_kernel(GemmParams p) {
     const int nchunks = ke > kb ? (ke - kb + BK - 1) / BK : 0;
 
     // Chunk bases (uniform): op(A) rows m0.., op(B) columns n0.., at k = kb.
-    const float *a_base = p.A + bz * p.strideA + (TA ? (int64_t)kb * p.lda + m0 : (int64_t)m0 * p.lda + kb);
-    const float *b_base = p.B + bz * p.strideB + (TB ? (int64_t)n0 * p.ldb + kb : (int64_t)kb * p.ldb + n0);
+    const T *a_base = reinterpret_cast<const T *>(p.A) + bz * p.strideA +
+                      (TA ? (int64_t)kb * p.lda + m0 : (int64_t)m0 * p.lda + kb);
+    const T *b_base = reinterpret_cast<const T *>(p.B) + bz * p.strideB +
+                      (TB ? (int64_t)n0 * p.ldb + kb : (int64_t)kb * p.ldb + n0);
     const int64_t a_step = TA ? (int64_t)BK * p.lda : BK;
     const int64_t b_step = TB ? BK : (int64_t)BK * p.ldb;
     const bool vec_a = p.vec_a != 0;
     const bool vec_b = p.vec_b != 0;
 
-    TileLoader<BM, NT, BK, !TA> la;
-    TileLoader<BN, NT, BK, TB> lb;
+    TileLoader<BM, NT, BK, !TA, T> la;
+    TileLoader<BN, NT, BK, TB, T> lb;
     la.init(p.lda, m0, p.m, tid);
     lb.init(p.ldb, n0, p.n, tid);
     auto row_wave = [](int o) { return ((o % HM) / 4) / TY_PER_WAVE; };
@@ -439,35 +441,43 @@ pam_gemm_kernel(GemmParams p) {
     }
 }
 
-template <int BM, int BN, int KW>
+template <int BM, int BN, int KW, typename T>
 static hipError_t launch_tile(bool ta, bool tb, const GemmParams &p, dim3 grid, hipStream_t stream) {
     const dim3 block(BM * BN / 64 * KW);
     if (!ta && !tb)
-        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, false, false>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, false, false, T>), grid, block, 0, stream, p);
     else if (!ta && tb)
-        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, false, true>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, false, true, T>), grid, block, 0, stream, p);
     else if (ta && !tb)
-        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, true, false>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, true, false, T>), grid, block, 0, stream, p);
     else
-        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, true, true>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_kernel<BM, BN, KW, true, true, T>), grid, block, 0, stream, p);
     return hipGetLastError();
 }
 
-hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, const GemmParams &p,
-                           hipStream_t stream) {
+template <typename T>
+static hipError_t launch_shape(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, const GemmParams &p,
+                               dim3 grid, hipStream_t stream) {
+    if (tile_m == 128 && tile_n == 128 && kgroups == 1)
+        return launch_tile<128, 128, 1, T>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 128 && tile_n == 64 && kgroups == 1)
+        return launch_tile<128, 64, 1, T>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 64 && tile_n == 64 && kgroups == 1)
+        return launch_tile<64, 64, 1, T>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 64 && tile_n == 64 && kgroups == 4)
+        return launch_tile<64, 64, 4, T>(trans_a, trans_b, p, grid, stream);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, bool bf16,
+                           const GemmParams &p, hipStream_t stream) {
     const int64_t items = (int64_t)p.whole + (int64_t)p.split_tiles * p.splits;
     if (items <= 0 || items > kMaxLaunchItems)
         return hipErrorInvalidValue;
     const dim3 grid((unsigned)items);
-    if (tile_m == 128 && tile_n == 128 && kgroups == 1)
-        return launch_tile<128, 128, 1>(trans_a, trans_b, p, grid, stream);
-    if (tile_m == 128 && tile_n == 64 && kgroups == 1)
-        return launch_tile<128, 64, 1>(trans_a, trans_b, p, grid, stream);
-    if (tile_m == 64 && tile_n == 64 && kgroups == 1)
-        return launch_tile<64, 64, 1>(trans_a, trans_b, p, grid, stream);
-    if (tile_m == 64 && tile_n == 64 && kgroups == 4)
-        return launch_tile<64, 64, 4>(trans_a, trans_b, p, grid, stream);
-    return hipErrorInvalidValue;
+    if (bf16)
+        return launch_shape<uint16_t>(tile_m, tile_n, kgroups, trans_a, trans_b, p, grid, stream);
+    return launch_shape<float>(tile_m, tile_n, kgroups, trans_a, trans_b, p, grid, stream);
 }
 
 // ---------------------------------------------------------------------------

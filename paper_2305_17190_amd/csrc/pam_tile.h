@@ -13,15 +13,21 @@
 
 namespace pamk {
 
+// float32 encodings of the operand elements: a float32 is its own encoding;
+// a bfloat16 (the high 16 bits of a float32) widens exactly by a shift.
+__device__ __forceinline__ uint32_t widen(float x) { return __float_as_uint(x); }
+__device__ __forceinline__ uint32_t widen(uint16_t h) { return (uint32_t)h << 16; }
+
 // An operand tile of D (rows of op(A), or columns of op(B)) x kChunkK, staged
-// through registers.  KCONTIG: element (o, kk) of chunk c sits at
+// through registers, from float32 or bfloat16 (T) elements.  KCONTIG: element (o, kk) of chunk c sits at
 // base + (o0 + o) * ld + k0 + kk (A with op N, B with op T); otherwise at
 // base + (k0 + kk) * ld + o0 + o (A with op T, B with op N).  Each thread
 // holds L groups of four elements consecutive in memory.  The byte offset of
 // each group from the chunk's base is fixed for the whole K loop, so the base
 // (uniform, in scalar registers) is the only address that moves.
-template <int D, int NT, int BK, bool KCONTIG>
+template <int D, int NT, int BK, bool KCONTIG, typename T = float>
 struct TileLoader {
+    static constexpr int ES = (int)sizeof(T);   // bytes per element
     static constexpr int L = D * BK / 4 / NT;
     static_assert(L >= 1 && D * BK / 4 == L * NT, "tile does not divide over the threads");
     uint4 v[L];
@@ -48,9 +54,9 @@ struct TileLoader {
             const int kk = grp_k(tid, r);
             if (KCONTIG) {
                 const int row = min(o0 + o, o_lim - 1) - o0;
-                boff[r] = (uint32_t)((row * ld + kk) * 4);
+                boff[r] = (uint32_t)((row * ld + kk) * ES);
             } else {
-                boff[r] = (uint32_t)((kk * ld + o) * 4);
+                boff[r] = (uint32_t)((kk * ld + o) * ES);
                 if (o0 + o + 3 >= o_lim)
                     edge |= 1u << r;
             }
@@ -59,7 +65,7 @@ struct TileLoader {
 
     // Load chunk elements [k0, k0 + BK) of the panel whose chunk base is
     // `base`.  Elements at k >= k_lim are zero (they must add nothing).
-    __device__ __forceinline__ void load(const float *__restrict__ base, int o0, int o_lim, int k0, int k_lim,
+    __device__ __forceinline__ void load(const T *__restrict__ base, int o0, int o_lim, int k0, int k_lim,
                                          bool vec, int tid) {
         const char *cb = reinterpret_cast<const char *>(base);
         if (vec && k0 + BK <= k_lim) {
@@ -67,7 +73,7 @@ struct TileLoader {
 #pragma unroll
             for (int r = 0; r < L; ++r) {
                 if (KCONTIG || !((edge >> r) & 1u))
-                    v[r] = *reinterpret_cast<const uint4 *>(cb + boff[r]);
+                    v[r] = load_group(cb + boff[r]);
                 else
                     v[r] = load_elements(cb, r, o0, o_lim, k0, k_lim, tid);
             }
@@ -78,23 +84,34 @@ struct TileLoader {
         }
     }
 
+    // Four consecutive elements at a 16-byte (float32) or 8-byte (bfloat16)
+    // aligned address, as float32 encodings.
+    static __device__ __forceinline__ uint4 load_group(const char *p) {
+        if constexpr (sizeof(T) == 4) {
+            return *reinterpret_cast<const uint4 *>(p);
+        } else {
+            const uint2 h = *reinterpret_cast<const uint2 *>(p);   // elements 0, 1 in h.x; 2, 3 in h.y
+            return make_uint4(h.x << 16, h.x & 0xFFFF0000u, h.y << 16, h.y & 0xFFFF0000u);
+        }
+    }
+
     // Group r element by element, with the K tail and (OCONTIG) the last
     // valid row applied.
     __device__ __forceinline__ uint4 load_elements(const char *cb, int r, int o0, int o_lim, int k0, int k_lim,
                                                    int tid) const {
-        const float *src = reinterpret_cast<const float *>(cb + boff[r]);
+        const T *src = reinterpret_cast<const T *>(cb + boff[r]);
         const int kk = grp_k(tid, r);
         uint32_t e[4];
         if (KCONTIG) {
 #pragma unroll
             for (int c = 0; c < 4; ++c)
-                e[c] = (k0 + kk + c < k_lim) ? __float_as_uint(src[c]) : 0u;
+                e[c] = (k0 + kk + c < k_lim) ? widen(src[c]) : 0u;
         } else {
             const int o = grp_o(tid, r);
-            const float *row = src - o;
+            const T *row = src - o;
 #pragma unroll
             for (int c = 0; c < 4; ++c)
-                e[c] = (k0 + kk < k_lim) ? __float_as_uint(row[min(o0 + o + c, o_lim - 1) - o0]) : 0u;
+                e[c] = (k0 + kk < k_lim) ? widen(row[min(o0 + o + c, o_lim - 1) - o0]) : 0u;
         }
         return make_uint4(e[0], e[1], e[2], e[3]);
     }

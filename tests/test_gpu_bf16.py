@@ -1,0 +1,104 @@
+"""PAM matrix products of bfloat16 operands (7-bit mantissas stored in half
+the bytes): the kernels widen each element exactly to float32 as they load
+it, so the product must equal the float32 product of the widened operands bit
+for bit (same plan), and the oracle's product within the GEMM tolerance."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import paper_2305_17190_amd as pam
+from gpu_util import check_gemm, device, note, oracle_gemm
+
+pytestmark = pytest.mark.gpu
+
+
+def bf16_bits(shape, seed, kinds=False):
+    """Seeded bfloat16 bit patterns: N(0,1) values rounded to bfloat16 by
+    torch's conversion, optionally with zeros, denormals and tiny normals."""
+    import torch
+    g = torch.Generator().manual_seed(seed)
+    x = torch.randn(shape, generator=g)
+    if kinds:
+        flat = x.view(-1)
+        n = flat.numel()
+        idx = torch.randperm(n, generator=g)[: max(3, n // 40)]
+        flat[idx[0::3]] = 0.0
+        flat[idx[1::3]] = 3e-39          # denormal, representable in bfloat16
+        flat[idx[2::3]] = 2e-38          # tiny normal
+    return x.to(torch.bfloat16)
+
+
+def widened(t16):
+    """float32 values of bfloat16 tensor elements: the 16 bits shifted up."""
+    import torch
+    bits = t16.cpu().view(torch.int16).numpy().view(np.uint16)
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+@pytest.mark.parametrize("m,n,k,batch,ta,tb,kinds", [
+    (203, 150, 333, 1, False, True, False),
+    (130, 200, 100, 2, True, False, True),
+    (96, 64, 4096, 3, False, False, False),
+    (70, 300, 50, 1, True, True, True),
+    (768, 192, 12608, 1, True, False, False),
+])
+def test_bf16_products(m, n, k, batch, ta, tb, kinds):
+    import torch
+    note(f"bf16 bmm m={m} n={n} k={k} batch={batch} ta={ta} tb={tb} kinds={kinds} plan={pam.plan(m, n, k, batch)}")
+    a16 = bf16_bits((batch, k, m) if ta else (batch, m, k), 2 * m + k, kinds).to(device())
+    b16 = bf16_bits((batch, n, k) if tb else (batch, k, n), 3 * n + k, kinds).to(device())
+    c16 = pam.bmm(a16, b16, trans_a=ta, trans_b=tb)
+    # the same product of the widened float32 operands: the same bits
+    c32 = pam.bmm(a16.float(), b16.float(), trans_a=ta, trans_b=tb)
+    assert torch.equal(c16.view(torch.int32), c32.view(torch.int32))
+    a, b = widened(a16), widened(b16)
+    lda, ldb = a.shape[-1], b.shape[-1]
+    c_ref, s_ref = oracle_gemm(a, b, ta, tb, m, n, k, lda, ldb, a[0].size, b[0].size, batches=list(range(batch)))
+    check_gemm(c16.cpu().numpy(), c_ref, s_ref, k, f"bf16 m={m} n={n} k={k}")
+
+
+def test_bf16_unaligned_rows_and_views():
+    # A starting 2 bytes past an 8-byte boundary and padded rows: the loader's
+    # element-by-element path
+    import torch
+    note("bf16 gemm on offset / padded views")
+    base = bf16_bits((1, 91 * 77 + 1), 5).to(device())[0]
+    a = base[1:].view(91, 77)[:, :75]                 # lda 77, not 8-byte aligned
+    b = bf16_bits((75, 33), 6).to(device())
+    c = pam.gemm(a, b)
+    c32 = pam.gemm(a.float(), b.float())
+    assert torch.equal(c.view(torch.int32), c32.view(torch.int32))
+
+
+def test_bf16_c_abi_workspace_modes():
+    import torch
+    lib = pam.load()
+    m, n, k, batch = 64, 48, 20000, 2
+    note(f"pam_gemm_batched_bf16 with and without a caller workspace m={m} n={n} k={k} batch={batch}")
+    a = bf16_bits((batch, m, k), 7).to(device())
+    b = bf16_bits((batch, k, n), 8).to(device())
+    size = ctypes.c_size_t()
+    assert lib.pam_gemm_workspace_size(m, n, k, batch, ctypes.byref(size)) == 0 and size.value > 0
+    ws = torch.empty(size.value, dtype=torch.uint8, device=device())
+    stream = torch.cuda.current_stream().cuda_stream
+    outs = []
+    for w, nbytes in ((None, 0), (ws.data_ptr(), size.value)):
+        c = torch.full((batch, m, n), float("nan"), device=device())
+        assert lib.pam_gemm_batched_bf16(0, 0, m, n, k, a.data_ptr(), k, m * k, b.data_ptr(), n, k * n,
+                                         c.data_ptr(), n, m * n, batch, w, nbytes, stream) == 0
+        outs.append(c)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0].view(torch.int32), outs[1].view(torch.int32))
+    assert torch.equal(outs[0].view(torch.int32), pam.bmm(a.float(), b.float()).view(torch.int32))
+
+
+def test_bf16_argument_rules():
+    import torch
+    a = torch.zeros((4, 4), dtype=torch.bfloat16, device=device())
+    with pytest.raises(TypeError):
+        pam.gemm(a, a.float())
+    with pytest.raises(ValueError):
+        pam.bmm(a[None], a[None], plan=(128, 128, 1))
+    with pytest.raises(ValueError):
+        pam.gemm(a, a, mantissa_bits=4)

@@ -65,7 +65,13 @@ typedef enum {
     PAM_ERROR_ALLOC = 4          /* stream-ordered workspace allocation failed */
 } pam_status_t;
 
+/* An int-sized enum.  Any other value is refused with PAM_ERROR_INVALID_VALUE;
+ * C++ sees a fixed underlying type, so such a value is still a valid object. */
+#ifdef __cplusplus
+typedef enum : int32_t { PAM_OP_N = 0, PAM_OP_T = 1 } pam_op_t;
+#else
 typedef enum { PAM_OP_N = 0, PAM_OP_T = 1 } pam_op_t;
+#endif
 
 /*
  * Elementwise PAM (Sec. 2.2): out[i] = a[i] .^ b[i] for 0 <= i < n.

@@ -26,7 +26,6 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Optional
 
 __all__ = ["mul", "pad", "palog2", "paexp2", "round_mantissa", "gemm", "bmm", "exact_grad", "plan",
            "device_info", "library_path", "load", "PamError"]

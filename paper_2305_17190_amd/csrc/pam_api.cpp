@@ -189,6 +189,16 @@ Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch) {
     return best[0];
 }
 
+// Output tiles of the smallest tile shape over the whole batch, at most
+// 2^40 (petabytes of output): the plan and launch arithmetic on tile counts
+// (times split counts and slots) then stays far inside int64.
+pam_status_t check_output_size(int64_t m, int64_t n, int64_t batch) {
+    const int64_t tiles = ceil_div(std::max<int64_t>(m, 1), 64) * ceil_div(std::max<int64_t>(n, 1), 64);
+    if (batch > 0 && tiles > ((int64_t)1 << 40) / batch)
+        return fail(PAM_ERROR_INVALID_VALUE, "too many output tiles (m * n * batch too large)");
+    return PAM_SUCCESS;
+}
+
 pam_status_t validate(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                       int64_t sa, const float *B, int64_t ldb, int64_t sb, const float *C, int64_t ldc, int64_t sc,
                       int64_t batch) {
@@ -202,6 +212,8 @@ pam_status_t validate(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     }
     if (m > kMaxDim || n > kMaxDim || k > kMaxDim)
         return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
+    if (check_output_size(m, n, batch) != PAM_SUCCESS)
+        return PAM_ERROR_INVALID_VALUE;
     if (sa < 0 || sb < 0 || sc < 0)
         return fail(PAM_ERROR_INVALID_VALUE, "batch strides must be >= 0");
     if (lda >= kMaxLd || ldb >= kMaxLd)
@@ -636,6 +648,8 @@ pam_status_t pam_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t ba
         return fail(PAM_ERROR_INVALID_VALUE, "m, n, k and batch must be >= 0");
     if (m > kMaxDim || n > kMaxDim || k > kMaxDim)
         return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
+    if (check_output_size(m, n, batch) != PAM_SUCCESS)
+        return PAM_ERROR_INVALID_VALUE;
     if (m == 0 || n == 0 || k == 0 || batch == 0)
         return PAM_SUCCESS;
     Layout L;
@@ -735,6 +749,10 @@ pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_p
         return fail(PAM_ERROR_INVALID_VALUE, "plan is NULL");
     if (m <= 0 || n <= 0 || k < 0 || batch <= 0)
         return fail(PAM_ERROR_INVALID_VALUE, "m, n, batch must be > 0 and k >= 0");
+    if (m > kMaxDim || n > kMaxDim || k > kMaxDim)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
+    if (check_output_size(m, n, batch) != PAM_SUCCESS)
+        return PAM_ERROR_INVALID_VALUE;
     const Plan p = choose_plan(m, n, std::max<int64_t>(k, 1), batch);
     plan->tile_m = p.tile_m;
     plan->tile_n = p.tile_n;

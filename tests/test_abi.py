@@ -232,3 +232,11 @@ def test_absurd_batch_is_refused_not_overflowed(lib):
     st, _ = _ws_size(lib, 1 << 30, 1 << 30, 64, 1 << 40)
     assert st == 1 and b"too many" in lib.pam_last_error()
     assert lib.pam_gemm_batched(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1 << 62, None) == 1
+    # every planning entry point applies the same bound (2^40 output tiles of 64 x 64)
+    with pytest.raises(pam.PamError, match="too many"):
+        pam.plan(1 << 30, 1 << 30, 64, 1 << 40)
+    with pytest.raises(pam.PamError, match="below 2"):
+        pam.plan(1 << 31, 4, 4)
+    # a large but launchable product (2^20 tiles of 128 x 128 per matrix) is planned
+    assert pam.plan(1 << 17, 1 << 17, 64, 4)[:2] in {(128, 128), (128, 64), (64, 64)}
+    assert _ws_size(lib, 1 << 17, 1 << 17, 64, 4)[0] == 0

@@ -139,32 +139,37 @@ struct TileLoader {
 
     // Scan the held elements.  Returns bit 0 when some element has exponent
     // field below 64 (zero, denormal, or "tiny": a normal number whose
-    // products can underflow) and bit 1 when some element needs the SPECIAL
-    // path (inf, NaN or |x| >= 2^64).
+    // products can underflow), bit 1 when some element needs the SPECIAL
+    // path (inf, NaN or |x| >= 2^64), and bit 2 + r when group r holds an
+    // element of the first kind.
     __device__ __forceinline__ uint32_t scan() const {
-        uint32_t hi = 0, lo = 0xFFFFFFFFu;
+        uint32_t hi = 0, groups = 0;
 #pragma unroll
         for (int r = 0; r < L; ++r) {
             const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+            uint32_t lo = 0xFFFFFFFFu;
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 const uint32_t ex = e[c] & kExpMask;
                 hi = max(hi, ex);
                 lo = min(lo, ex);
             }
+            if (lo < (64u << 23))
+                groups |= 1u << r;
         }
-        return (lo < (64u << 23) ? 1u : 0u) | (hi >= (191u << 23) ? 2u : 0u);
+        return (groups != 0u ? 1u : 0u) | (hi >= (191u << 23) ? 2u : 0u) | (groups << 2);
     }
 
     // Write the chunk into LDS buffer s, k-major: s[plane][kk][o].  A: plane 0
     // aM (1 + M), plane 1 m (+-2^E or +-0), plane 2 a itself; B: plane 0 b'
-    // (b - bias, zero and denormal b as a signed zero first).  When
-    // `has_low`, an element at chunk step k with exponent field below 64 sets
-    // bit k % 16 of mask[(k / 16) * (b_slot + 1) + w], and a normal one among
-    // them (tiny) also bit 16 + k % 16; w is the row wave that reads the
-    // element (A) or b_slot (B).
+    // (b - bias, zero and denormal b as a signed zero first).  In the groups
+    // flagged in `low_groups` (bit r: group r, as scan() reports), an element
+    // at chunk step k with exponent field below 64 sets bit k % 16 of
+    // mask[(k / 16) * (b_slot + 1) + w], and a normal one among them (tiny)
+    // also bit 16 + k % 16; w is the row wave that reads the element (A) or
+    // b_slot (B).
     template <int LDS_LD, typename RowWave>
-    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], bool is_b, int tid, bool has_low,
+    __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], bool is_b, int tid, uint32_t low_groups,
                                           uint32_t *mask, int b_slot, RowWave row_wave) const {
 #pragma unroll
         for (int r = 0; r < L; ++r) {
@@ -207,7 +212,9 @@ struct TileLoader {
                     *reinterpret_cast<uint4 *>(&s[2][kk][o]) = v[r];
                 }
             }
-            if (has_low) {
+            // Rare: a branch per group, which the wave skips unless one of
+            // its lanes holds such an element in this group.
+            if ((low_groups >> r) & 1u) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const uint32_t ex = e[c] & kExpMask;

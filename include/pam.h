@@ -41,10 +41,16 @@
  *   - Arguments are validated before anything is launched; on failure the
  *     call returns PAM_ERROR_INVALID_VALUE and pam_last_error() says why.
  *   - Output regions overlapping an input are undefined (not checked), except
- *     that pam_mul may run in place (out == a or out == b).
+ *     that the elementwise calls (pam_mul, pam_pad, pam_palog2, pam_paexp2,
+ *     pam_round_mantissa) may run in place (out == a or out == b).
  *   - Split-K plans take a temporary partial-sum buffer from the
- *     stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`);
- *     nothing stays allocated when the call returns.
+ *     stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`),
+ *     freed (stream-ordered) before the call returns, unless the caller
+ *     passes a workspace (the *_ws and bf16 entry points).  On its first
+ *     call on a device the library sets that device's default memory pool
+ *     to keep freed memory for reuse (hipMemPoolAttrReleaseThreshold =
+ *     UINT64_MAX), a process-wide setting that spares a return to the driver
+ *     at every synchronisation; hipMemPoolTrimTo gives the memory back.
  */
 #ifndef PAM_H_
 #define PAM_H_

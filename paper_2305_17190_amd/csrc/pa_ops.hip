@@ -110,12 +110,14 @@ struct RoundOp {
 // 16-byte groups, read and written with non-temporal hints (a stream touches
 // each byte once), one group per thread: with a workgroup per 256 groups the
 // chip keeps far more loads in flight than a short grid-stride loop would.
-// The grid-stride loop only runs past kMaxBlocks workgroups.
+// The grid-stride loop only runs past kMaxBlocks workgroups.  The pointers
+// may alias (every op may run in place: each thread reads its elements
+// before it writes them), so none is marked __restrict__.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 template <typename Op>
-__global__ void __launch_bounds__(256) binary_vec4_kernel(const u32x4 *__restrict__ a, const u32x4 *__restrict__ b,
-                                                          u32x4 *__restrict__ out, int64_t n4) {
+__global__ void __launch_bounds__(256) binary_vec4_kernel(const u32x4 *a, const u32x4 *b, u32x4 *out,
+                                                          int64_t n4) {
     const Op op;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
@@ -127,9 +129,8 @@ __global__ void __launch_bounds__(256) binary_vec4_kernel(const u32x4 *__restric
 }
 
 template <typename Op>
-__global__ void __launch_bounds__(256) binary_scalar_kernel(const uint32_t *__restrict__ a,
-                                                            const uint32_t *__restrict__ b,
-                                                            uint32_t *__restrict__ out, int64_t n) {
+__global__ void __launch_bounds__(256) binary_scalar_kernel(const uint32_t *a, const uint32_t *b,
+                                                            uint32_t *out, int64_t n) {
     const Op op;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
@@ -138,8 +139,8 @@ __global__ void __launch_bounds__(256) binary_scalar_kernel(const uint32_t *__re
 }
 
 template <typename Op>
-__global__ void __launch_bounds__(256) unary_vec4_kernel(const u32x4 *__restrict__ a, u32x4 *__restrict__ out,
-                                                         int64_t n4, Op op) {
+__global__ void __launch_bounds__(256) unary_vec4_kernel(const u32x4 *a, u32x4 *out, int64_t n4,
+                                                         Op op) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
         const u32x4 x = __builtin_nontemporal_load(a + i);
@@ -149,8 +150,8 @@ __global__ void __launch_bounds__(256) unary_vec4_kernel(const u32x4 *__restrict
 }
 
 template <typename Op>
-__global__ void __launch_bounds__(256) unary_scalar_kernel(const uint32_t *__restrict__ a, uint32_t *__restrict__ out,
-                                                           int64_t n, Op op) {
+__global__ void __launch_bounds__(256) unary_scalar_kernel(const uint32_t *a, uint32_t *out, int64_t n,
+                                                           Op op) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
         __builtin_nontemporal_store(op(__builtin_nontemporal_load(a + i)), out + i);

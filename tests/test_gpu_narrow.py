@@ -33,6 +33,18 @@ def test_rounding_bit_exact(b):
     assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
 
 
+def test_rounding_in_place_and_unaligned():
+    note("round_mantissa in place and on a view starting 4 bytes in")
+    x = np.concatenate([wl.special_bit_patterns(), wl.random_bit_patterns(4099, 650)])
+    d = to_dev(x)
+    out = pam.round_mantissa(d, 5, out=d)
+    assert out.data_ptr() == d.data_ptr()
+    assert np.array_equal(d.cpu().numpy().view(np.uint32), pam_ref.round_mantissa_ref(x, 5).view(np.uint32))
+    d = to_dev(x)
+    got = pam.round_mantissa(d[1:], 9).cpu().numpy()
+    assert np.array_equal(got.view(np.uint32), pam_ref.round_mantissa_ref(x[1:], 9).view(np.uint32))
+
+
 def narrow_case(ta, tb, m, n, k, bits, seed, batch=1, kind="normal"):
     g = np.random.default_rng(seed)
     ar, ac = (k, m) if ta else (m, k)

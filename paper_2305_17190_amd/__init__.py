@@ -17,8 +17,9 @@ device every call raises.
 Matrix arguments are float32 HIP tensors whose last dimension is contiguous
 (row stride = leading dimension).  Products that split K take their
 workspace from torch's caching allocator (the library's ``*_ws`` entry
-points), so a call never waits for the GPU.  op(X) = X^T when trans_x is True.  The
-linear layer Y = X W^T is ``gemm(X, W, trans_b=True)``; its backward
+points), so a call never waits for the GPU.  Every tensor of a call must be
+on one device, which the call makes current.  op(X) = X^T when trans_x is
+True.  The linear layer Y = X W^T is ``gemm(X, W, trans_b=True)``; its backward
 products (approximate derivative, Table 1 of the paper) are
 ``gemm(dY, W)`` and ``gemm(dY, X, trans_a=True)``.
 """
@@ -164,6 +165,14 @@ def _require(t, name: str, ndim: int, bf16_ok: bool = False):
         raise ValueError(f"{name} must have a contiguous last dimension")
 
 
+def _same_device(ref, *named):
+    """The library launches on the current HIP device: every tensor of a call
+    must live on the first operand's device (made current for the call)."""
+    for name, t in named:
+        if t is not None and t.device != ref.device:
+            raise ValueError(f"{name} is on {t.device}, the first operand on {ref.device}")
+
+
 def _elementwise_args(tensors, out):
     torch = _torch()
     for name, t in tensors:
@@ -171,6 +180,7 @@ def _elementwise_args(tensors, out):
         if not t.is_contiguous():
             raise ValueError(f"{name} must be contiguous")
     a = tensors[0][1]
+    _same_device(a, *tensors[1:])
     for name, t in tensors[1:]:
         if t.shape != a.shape:
             raise ValueError(f"shape mismatch {tuple(a.shape)} vs {tuple(t.shape)}")
@@ -185,35 +195,40 @@ def _elementwise_args(tensors, out):
 def mul(a, b, out=None):
     """Elementwise PAM of two equally shaped contiguous float32 tensors."""
     a, out = _elementwise_args((("a", a), ("b", b)), out)
-    _check(load().pam_mul(a.data_ptr(), b.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
+    with _torch().cuda.device(a.device):
+        _check(load().pam_mul(a.data_ptr(), b.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
     return out
 
 
 def pad(a, b, out=None):
     """Elementwise piecewise affine division a ./ b (Sec. 2.3)."""
     a, out = _elementwise_args((("a", a), ("b", b)), out)
-    _check(load().pam_pad(a.data_ptr(), b.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
+    with _torch().cuda.device(a.device):
+        _check(load().pam_pad(a.data_ptr(), b.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
     return out
 
 
 def palog2(a, out=None):
     """Elementwise palog2(a) = E + M (Sec. 2.3), rounded to float32."""
     a, out = _elementwise_args((("a", a),), out)
-    _check(load().pam_palog2(a.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
+    with _torch().cuda.device(a.device):
+        _check(load().pam_palog2(a.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
     return out
 
 
 def paexp2(a, out=None):
     """Elementwise paexp2(a) = 2^floor(a) (1 + a - floor(a)) (Sec. 2.3), rounded to float32."""
     a, out = _elementwise_args((("a", a),), out)
-    _check(load().pam_paexp2(a.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
+    with _torch().cuda.device(a.device):
+        _check(load().pam_paexp2(a.data_ptr(), out.data_ptr(), a.numel(), _stream_handle(a)))
     return out
 
 
 def round_mantissa(a, bits: int, out=None):
     """Elementwise rounding to ``bits`` mantissa bits (App. "PAM with Narrower Mantissas")."""
     a, out = _elementwise_args((("a", a),), out)
-    _check(load().pam_round_mantissa(a.data_ptr(), out.data_ptr(), a.numel(), int(bits), _stream_handle(a)))
+    with _torch().cuda.device(a.device):
+        _check(load().pam_round_mantissa(a.data_ptr(), out.data_ptr(), a.numel(), int(bits), _stream_handle(a)))
     return out
 
 
@@ -259,18 +274,20 @@ def gemm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, mantissa_
         _require(out, "out", 2)
         if tuple(out.shape) != (m, n):
             raise ValueError(f"out must be {m}x{n}")
+    _same_device(A, ("B", B), ("out", out))
     ta = PAM_OP_T if trans_a else PAM_OP_N
     tb = PAM_OP_T if trans_b else PAM_OP_N
-    ws, ws_bytes, keep = _workspace("gemm", (m, n, k, 1), A.device)
     lib = load()
-    if bf16:
-        _check(lib.pam_gemm_batched_bf16(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
-                                         out.data_ptr(), _ld(out), 0, 1, ws, ws_bytes, _stream_handle(A)))
-    else:
-        _check(lib.pam_gemm_batched_ws(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
-                                       out.data_ptr(), _ld(out), 0, 1, int(mantissa_bits), ws, ws_bytes,
-                                       _stream_handle(A)))
-    del keep
+    with torch.cuda.device(A.device):
+        ws, ws_bytes, keep = _workspace("gemm", (m, n, k, 1), A.device)
+        if bf16:
+            _check(lib.pam_gemm_batched_bf16(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
+                                             out.data_ptr(), _ld(out), 0, 1, ws, ws_bytes, _stream_handle(A)))
+        else:
+            _check(lib.pam_gemm_batched_ws(ta, tb, m, n, k, A.data_ptr(), _ld(A), 0, B.data_ptr(), _ld(B), 0,
+                                           out.data_ptr(), _ld(out), 0, 1, int(mantissa_bits), ws, ws_bytes,
+                                           _stream_handle(A)))
+        del keep
     return out
 
 
@@ -279,8 +296,9 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
 
     ``plan`` = (tile_m, tile_n, splits[, kgroups[, whole_tiles]]) forces a
     tiling (tests and tuning); ``whole_tiles`` tiles, counted from the first,
-    then take the whole K and only the rest are split.  ``mantissa_bits`` < 23 rounds every operand element to that
-    many mantissa bits first (the library then picks the plan).
+    then take the whole K and only the rest are split.  ``mantissa_bits`` <
+    23 rounds every operand element to that many mantissa bits first (the
+    library then picks the plan).
     """
     torch = _torch()
     _require(A, "A", 3, bf16_ok=True)
@@ -296,29 +314,30 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
         _require(out, "out", 3)
         if tuple(out.shape) != (batch, m, n):
             raise ValueError(f"out must be {batch}x{m}x{n}")
+    _same_device(A, ("B", B), ("out", out))
     ta = PAM_OP_T if trans_a else PAM_OP_N
     tb = PAM_OP_T if trans_b else PAM_OP_N
     args = (ta, tb, m, n, k, A.data_ptr(), _ld(A), A.stride(0), B.data_ptr(), _ld(B), B.stride(0),
             out.data_ptr(), _ld(out), out.stride(0), batch)
-    lib = load()
-    if bf16:
-        if plan is not None:
-            raise ValueError("bfloat16 operands take the library's plan")
-        ws, ws_bytes, keep = _workspace("gemm", (m, n, k, batch), A.device)
-        _check(lib.pam_gemm_batched_bf16(*args, ws, ws_bytes, _stream_handle(A)))
-        del keep
-    elif plan is None:
-        ws, ws_bytes, keep = _workspace("gemm", (m, n, k, batch), A.device)
-        _check(lib.pam_gemm_batched_ws(*args, int(mantissa_bits), ws, ws_bytes, _stream_handle(A)))
-        del keep
-    elif mantissa_bits != 23:
+    if bf16 and plan is not None:
+        raise ValueError("bfloat16 operands take the library's plan")
+    if plan is not None and mantissa_bits != 23:
         raise ValueError("plan and mantissa_bits cannot be combined")
-    else:
-        if not 3 <= len(plan) <= 5:
-            raise ValueError("plan is (tile_m, tile_n, splits[, kgroups[, whole_tiles]])")
-        full = tuple(plan) + (1, 0)[len(plan) - 3:]
-        p = _Plan(*full)
-        _check(lib.pam_gemm_batched_with_plan(*args, ctypes.byref(p), _stream_handle(A)))
+    if plan is not None and not 3 <= len(plan) <= 5:
+        raise ValueError("plan is (tile_m, tile_n, splits[, kgroups[, whole_tiles]])")
+    lib = load()
+    with torch.cuda.device(A.device):
+        if plan is not None:
+            full = tuple(plan) + (1, 0)[len(plan) - 3:]
+            p = _Plan(*full)
+            _check(lib.pam_gemm_batched_with_plan(*args, ctypes.byref(p), _stream_handle(A)))
+            return out
+        ws, ws_bytes, keep = _workspace("gemm", (m, n, k, batch), A.device)
+        if bf16:
+            _check(lib.pam_gemm_batched_bf16(*args, ws, ws_bytes, _stream_handle(A)))
+        else:
+            _check(lib.pam_gemm_batched_ws(*args, int(mantissa_bits), ws, ws_bytes, _stream_handle(A)))
+        del keep
     return out
 
 
@@ -342,11 +361,13 @@ def exact_grad(A, B, Mod, trans_a: bool = False, out=None):
         _require(out, "out", 2)
         if tuple(out.shape) != (m, n):
             raise ValueError(f"out must be {m}x{n}")
-    ws, ws_bytes, keep = _workspace("exact", (m, n, k), A.device)
-    _check(load().pam_gemm_exact_grad_ws(PAM_OP_T if trans_a else PAM_OP_N, m, n, k, A.data_ptr(), _ld(A),
-                                         B.data_ptr(), _ld(B), Mod.data_ptr(), _ld(Mod), out.data_ptr(), _ld(out),
-                                         ws, ws_bytes, _stream_handle(A)))
-    del keep
+    _same_device(A, ("B", B), ("Mod", Mod), ("out", out))
+    with torch.cuda.device(A.device):
+        ws, ws_bytes, keep = _workspace("exact", (m, n, k), A.device)
+        _check(load().pam_gemm_exact_grad_ws(PAM_OP_T if trans_a else PAM_OP_N, m, n, k, A.data_ptr(), _ld(A),
+                                             B.data_ptr(), _ld(B), Mod.data_ptr(), _ld(Mod), out.data_ptr(),
+                                             _ld(out), ws, ws_bytes, _stream_handle(A)))
+        del keep
     return out
 
 

@@ -32,6 +32,14 @@ from . import gemm as _gemm
 __all__ = ["pam_linear", "pam_matmul", "PAMLinear"]
 
 
+def _float32(**named) -> None:
+    """The wrappers' gradients are float32 products: refuse other dtypes up
+    front rather than in the backward pass."""
+    for name, t in named.items():
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError(f"{name} must be float32, got {t.dtype}")
+
+
 def _last_contiguous(t: torch.Tensor) -> torch.Tensor:
     """t itself when its rows are dense and non-overlapping (a valid leading
     dimension for the C ABI), else a contiguous copy."""
@@ -85,6 +93,7 @@ def pam_linear(x: torch.Tensor, weight: torch.Tensor, bias: torch.Tensor = None,
         raise ValueError('derivative must be "approximate" or "exact"')
     if derivative == "exact" and mantissa_bits != 23:
         raise ValueError("the exact derivative takes full float32 mantissas")
+    _float32(x=x, weight=weight, bias=bias)
     lead = x.shape[:-1]
     y = _PAMLinearFn.apply(x.reshape(-1, x.shape[-1]), weight, bias, int(mantissa_bits), derivative == "exact")
     return y.reshape(*lead, weight.shape[0])
@@ -113,6 +122,7 @@ class _PAMBmmFn(torch.autograd.Function):
 
 def pam_matmul(a: torch.Tensor, b: torch.Tensor, mantissa_bits: int = 23) -> torch.Tensor:
     """``a .^ b`` for 2-D or batched 3-D operands (leading batch dimension)."""
+    _float32(a=a, b=b)
     if a.dim() == 2 and b.dim() == 2:
         return _PAMBmmFn.apply(a.unsqueeze(0), b.unsqueeze(0), int(mantissa_bits)).squeeze(0)
     if a.dim() == 3 and b.dim() == 3:

@@ -164,6 +164,11 @@ def test_autograd_wrappers_refuse_cpu_tensors():
         lin(torch.ones(2, 4))
     with pytest.raises(pam.PamError):
         pam_matmul(torch.ones(2, 2), torch.ones(2, 2))
+    # float32 only (the gradients are float32 products), refused before any call
+    with pytest.raises(TypeError):
+        lin(torch.ones(2, 4, dtype=torch.bfloat16))
+    with pytest.raises(TypeError):
+        pam_matmul(torch.ones(2, 2, dtype=torch.float64), torch.ones(2, 2))
 
 
 def test_exact_grad_rejects_bad_arguments(lib):

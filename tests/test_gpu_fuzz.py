@@ -1,13 +1,15 @@
 """Seeded randomized parity sweep of the PAM matrix product against the C
 oracle: random sizes (ragged in every dimension), transposes, batch counts,
 padded leading dimensions and batch strides, every tile shape, random split
-counts and whole-tile counts (hybrid plans), plus the library's own plan.
-Each case is compared element by element within the GEMM tolerance."""
+counts and whole-tile counts (hybrid plans), plus the library's own plan;
+then the same with narrow-mantissa and bfloat16 operands.  Each case is
+compared element by element within the GEMM tolerance."""
 import numpy as np
 import pytest
 
 import paper_2305_17190_amd as pam
 from gpu_util import check_gemm, device, note, oracle_gemm, to_dev
+from oracle import pam_ref
 
 pytestmark = pytest.mark.gpu
 
@@ -64,3 +66,47 @@ def test_random_products(case):
     assert np.all(np.isnan(got[:, :, n:])), "wrote outside the output's columns"
     c_ref, s_ref = oracle_gemm(a_buf, b_buf, ta, tb, m, n, k, lda, ldb, sa, sb, batches=list(range(batch)))
     check_gemm(got[:, :, :n], c_ref, s_ref, k, f"fuzz {case}")
+
+
+NARROW_CASES = 40
+
+
+@pytest.mark.parametrize("case", range(NARROW_CASES))
+def test_random_narrow_and_bfloat16_products(case):
+    # The same random sizes, transposes and padded layouts with operands of
+    # fewer mantissa bits: float32 elements rounded to 0-10 mantissa bits by
+    # the kernels, or bfloat16 elements widened exactly as they are loaded.
+    # The oracle takes the rounded (resp. widened) float32 values.
+    import torch
+    rng = np.random.default_rng(5000 + case)
+    m, n, k, batch, ta, tb, pad, _ = draw(rng)
+    bf16 = case % 2 == 1
+    bits = 7 if bf16 else int(rng.choice([0, 3, 4, 7, 10]))
+    a_rows, a_cols = (k, m) if ta else (m, k)
+    b_rows, b_cols = (n, k) if tb else (k, n)
+    lda, ldb = a_cols + pad[0], b_cols + pad[1]
+    sa, sb = (a_rows + 1) * lda, (b_rows + 2) * ldb
+    a_buf = rng.standard_normal(batch * sa).astype(np.float32)
+    b_buf = (rng.standard_normal(batch * sb) * 0.1).astype(np.float32)
+    if case % 4 < 2:                                       # zeros, denormals and tiny values
+        for buf in (a_buf, b_buf):
+            idx = rng.choice(buf.size, size=max(1, buf.size // 50), replace=False)
+            buf[idx[0::3]] = 0.0
+            buf[idx[1::3]] = np.float32(3e-39)
+            buf[idx[2::3]] = np.float32(1.5e-38)
+    note(f"fuzz narrow {case}: m={m} n={n} k={k} batch={batch} ta={ta} tb={tb} pad={pad} "
+         f"{'bfloat16' if bf16 else f'bits={bits}'}")
+    if bf16:
+        a16 = torch.from_numpy(a_buf).to(torch.bfloat16)
+        b16 = torch.from_numpy(b_buf).to(torch.bfloat16)
+        a_ref = (a16.view(torch.int16).numpy().view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+        b_ref = (b16.view(torch.int16).numpy().view(np.uint16).astype(np.uint32) << 16).view(np.float32)
+        da, db = a16.to(device()), b16.to(device())
+    else:
+        a_ref, b_ref = pam_ref.round_mantissa_ref(a_buf, bits), pam_ref.round_mantissa_ref(b_buf, bits)
+        da, db = to_dev(a_buf), to_dev(b_buf)
+    da = torch.as_strided(da, (batch, a_rows, a_cols), (sa, lda, 1))
+    db = torch.as_strided(db, (batch, b_rows, b_cols), (sb, ldb, 1))
+    c = pam.bmm(da, db, trans_a=ta, trans_b=tb, mantissa_bits=bits).cpu().numpy()
+    c_ref, s_ref = oracle_gemm(a_ref, b_ref, ta, tb, m, n, k, lda, ldb, sa, sb, batches=list(range(batch)))
+    check_gemm(c, c_ref, s_ref, k, f"fuzz narrow {case}")

@@ -252,8 +252,14 @@ pam_gemm_kernel(GemmParams p) {
     constexpr int NT = NTG * KW;
     constexpr int NW = NT / 64;
     constexpr int NRW = NTG / 64;          // waves per k-group
-    constexpr int TXN = BN / 8;            // threads along n
-    constexpr int TY_PER_WAVE = 64 / TXN;  // micro-tile rows (of 2 x 4) per wave
+    // A k-group's waves form a WR x WC grid, each wave 8 x 8 threads (a
+    // 64 x 64 block of outputs when both operands' halves are counted): a
+    // k step then reads the fewest operand values per wave, so one zero or
+    // tiny value moves as few waves' steps off the two-op path as possible.
+    constexpr int WC = BN / 64;            // wave columns
+    constexpr int WR = NRW / WC;           // wave rows
+    constexpr int NSLOT = WR + WC;         // step-mask words per k-group: one per wave row, one per wave column
+    static_assert(WC >= 1 && WR * WC == NRW && BM / 64 == WR, "waves do not tile the output tile");
     constexpr int HM = BM / 2;
     constexpr int HN = BN / 2;
     constexpr int LDA = BM + 4;            // padded LDS rows, 16-byte aligned
@@ -267,17 +273,20 @@ pam_gemm_kernel(GemmParams p) {
     constexpr int kRedWords = KW > 1 ? KW * BM * LDR : 0;
     __shared__ __attribute__((aligned(16))) uint32_t smem[kTileWords > kRedWords ? kTileWords : kRedWords];
     __shared__ uint32_t sVote[NW];                 // chunk needs the SPECIAL path
-    __shared__ uint32_t sMask[2][KW * (NRW + 1)];  // [chunk parity] low / tiny bits per (group, row wave / B)
+    __shared__ uint32_t sMask[2][KW * NSLOT];      // [chunk parity] low / tiny bits per (group, wave row / wave column)
     uint32_t (*sA)[BK][LDA] = reinterpret_cast<uint32_t (*)[BK][LDA]>(smem);             // plane 0 aM, 1 m, 2 a
     uint32_t (*sB)[BK][LDB] = reinterpret_cast<uint32_t (*)[BK][LDB]>(smem + 3 * BK * LDA);  // b'
 
     const int tid = threadIdx.x;
     const int grp = tid / NTG;
     const int t = tid % NTG;
-    const int tx = t % TXN;
-    const int ty = t / TXN;
     const int wave = tid >> 6;
-    const int rwave = t >> 6;
+    const int gwave = t >> 6;              // wave within the k-group
+    const int wr = gwave / WC;
+    const int wc = gwave % WC;
+    const int lane = tid & 63;
+    const int tx = wc * 8 + (lane & 7);    // micro-tile column group (of 4, in each half)
+    const int ty = wr * 8 + (lane >> 3);   // micro-tile row group
     // Work item -> (tile, K range): whole-K tiles first, then the K slices of
     // the split tiles, slice by slice (neighbouring items share operand rows).
     const uint32_t item = blockIdx.x;
@@ -311,7 +320,8 @@ pam_gemm_kernel(GemmParams p) {
     TileLoader<BN, NT, BK, TB, T> lb;
     la.init(p.lda, m0, p.m, tid);
     lb.init(p.ldb, n0, p.n, tid);
-    auto row_wave = [](int o) { return ((o % HM) / 4) / TY_PER_WAVE; };
+    auto a_slot = [](int o) { return ((o % HM) / 4) / 8; };        // wave row reading tile row o
+    auto b_slot = [](int o) { return WR + ((o % HN) / 4) / 8; };   // wave column reading tile column o
 
     float acc[8][8];
 #pragma unroll
@@ -320,7 +330,7 @@ pam_gemm_kernel(GemmParams p) {
         for (int j = 0; j < 8; ++j)
             acc[i][j] = 0.0f;
 
-    if (tid < 2 * KW * (NRW + 1))
+    if (tid < 2 * KW * NSLOT)
         (&sMask[0][0])[tid] = 0u;
 
     if (nchunks > 0) {
@@ -339,8 +349,8 @@ pam_gemm_kernel(GemmParams p) {
         const uint64_t sp = __ballot((fa | fb) & 2u);
         uint32_t *mask = sMask[c & 1];
         __syncthreads();   // every wave is done reading the previous chunk (and zeroing this mask)
-        la.template store<LDA>(sA, false, tid, fa >> 2, mask, NRW, row_wave);
-        lb.template store<LDB>(sB, true, tid, fb >> 2, mask, NRW, row_wave);
+        la.template store<LDA>(sA, false, tid, fa >> 2, mask, NSLOT, a_slot);
+        lb.template store<LDB>(sB, true, tid, fb >> 2, mask, NSLOT, b_slot);
         if ((tid & 63) == 0)
             sVote[wave] = sp ? 1u : 0u;
         __syncthreads();
@@ -353,8 +363,8 @@ pam_gemm_kernel(GemmParams p) {
         // Bits 0..15: the wave's k steps with an operand of exponent field
         // below 64; bits 16..31: those among them with a tiny normal one.
         const uint32_t low =
-            __builtin_amdgcn_readfirstlane(mask[grp * (NRW + 1) + rwave] | mask[grp * (NRW + 1) + NRW]);
-        if (tid < KW * (NRW + 1))
+            __builtin_amdgcn_readfirstlane(mask[grp * NSLOT + wr] | mask[grp * NSLOT + WR + wc]);
+        if (tid < KW * NSLOT)
             sMask[(c + 1) & 1][tid] = 0u;   // next chunk's masks; last read one chunk ago
 
         if (c + 1 < nchunks) {

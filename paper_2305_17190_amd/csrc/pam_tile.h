@@ -165,12 +165,12 @@ struct TileLoader {
     // (b - bias, zero and denormal b as a signed zero first).  In the groups
     // flagged in `low_groups` (bit r: group r, as scan() reports), an element
     // at chunk step k with exponent field below 64 sets bit k % 16 of
-    // mask[(k / 16) * (b_slot + 1) + w], and a normal one among them (tiny)
-    // also bit 16 + k % 16; w is the row wave that reads the element (A) or
-    // b_slot (B).
-    template <int LDS_LD, typename RowWave>
+    // mask[(k / 16) * slots + slot_of(o)], and a normal one among them (tiny)
+    // also bit 16 + k % 16; slot_of(o) names the waves that read the element
+    // of tile row (A) or column (B) o.
+    template <int LDS_LD, typename SlotOf>
     __device__ __forceinline__ void store(uint32_t (*s)[BK][LDS_LD], bool is_b, int tid, uint32_t low_groups,
-                                          uint32_t *mask, int b_slot, RowWave row_wave) const {
+                                          uint32_t *mask, int slots, SlotOf slot_of) const {
 #pragma unroll
         for (int r = 0; r < L; ++r) {
             const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
@@ -221,7 +221,7 @@ struct TileLoader {
                     if (ex < (64u << 23)) {
                         const int k = KCONTIG ? kk + c : kk;
                         const uint32_t bit = 1u << (k % 16);
-                        atomicOr(&mask[(k / 16) * (b_slot + 1) + (is_b ? b_slot : row_wave(KCONTIG ? o : o + c))],
+                        atomicOr(&mask[(k / 16) * slots + slot_of(KCONTIG ? o : o + c)],
                                  ex != 0u ? (bit | (bit << 16)) : bit);
                     }
                 }

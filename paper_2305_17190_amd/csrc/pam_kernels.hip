@@ -340,6 +340,11 @@ pam_gemm_kernel(GemmParams p) {
 
     const int k_first = grp * KPG;
     for (int c = 0; c < nchunks; ++c) {
+        // The chunk's staging runs at a raised wave priority, so that a
+        // workgroup reaches its barriers sooner while other workgroups'
+        // waves compute (measured +0.3-0.9%); the step loops run at the
+        // base priority.
+        __builtin_amdgcn_s_setprio(1);
         if (p.round_drop != 0) {
             la.round_mantissa(p.round_drop);
             lb.round_mantissa(p.round_drop);
@@ -373,6 +378,7 @@ pam_gemm_kernel(GemmParams p) {
             lb.load(b_base + (c + 1) * b_step, n0, p.n, k0, ke, vec_b, tid);
         }
 
+        __builtin_amdgcn_s_setprio(0);
         const uint32_t (*cA)[BK][LDA] = sA;
         const uint32_t (*cB)[BK][LDB] = sB;
         // The wave's k steps of this chunk as four bit sets, taken by four

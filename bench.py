@@ -59,7 +59,8 @@ def committed_traffic(workload: str, form: str):
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}_{form}.md")
     if not os.path.exists(path):
         return None
-    text = open(path).read()
+    with open(path) as f:
+        text = f.read()
     sha = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
     val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not sha or not val or sha.group(1) != kernel_source_digest():

@@ -167,8 +167,8 @@ pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_p
 
 /*
  * pam_gemm_batched with an explicit plan (for tests and tuning).
- * (tile_m, tile_n, kgroups) is (128,128,1), (128,64,1), (64,64,1) or
- * (64,64,4); 1 <= splits <= 64; whole_tiles >= 0.  The result is the same
+ * (tile_m, tile_n, kgroups) is (128,128,1), (128,64,1), (128,64,2),
+ * (64,64,1) or (64,64,4); 1 <= splits <= 64; whole_tiles >= 0.  The result is the same
  * product as with the automatic plan, up to float32 summation order.  A plan
  * with 0 < whole_tiles < tiles runs as one launch and fails with
  * PAM_ERROR_INVALID_VALUE when its workgroups exceed 2^24 - 1.

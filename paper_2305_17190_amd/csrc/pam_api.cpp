@@ -53,12 +53,14 @@ struct Shape {
     int per_cu;     // workgroups resident per compute unit (register budget)
     double rate;    // PAM-MACs per second with every compute unit full (fitted to MI355X runs)
 };
-// 128 x 128 and 128 x 64 tiles with one k-group; 64 x 64 tiles with one
-// k-group, or whose four waves split each chunk's k steps (four times the
-// waves without partial sums in HBM, at twice the staging work per MAC).
-// The 128 x 128 tile holds three waves per SIMD, the others two.
+// 128 x 128 and 128 x 64 tiles with one k-group; 128 x 64 tiles whose two
+// k-groups split each chunk's k steps, and 64 x 64 tiles with one or four
+// (more waves without partial sums in HBM: the groups add their partial
+// tiles in LDS, at more staging work per MAC).  The 128 x 128 tile holds
+// three waves per SIMD, the others two.
 const Shape kShapes[] = {{128, 128, 1, 4, 3, 26.67e12},
                          {128, 64, 1, 2, 4, 20.49e12},
+                         {128, 64, 2, 4, 2, 19.6e12},
                          {64, 64, 1, 1, 8, 19.64e12},
                          {64, 64, 4, 4, 2, 15.99e12}};
 constexpr int kComputeUnits = 256;
@@ -774,10 +776,12 @@ pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB, int64_
     const bool tile_ok = (plan->kgroups == 1 && ((plan->tile_m == 128 && plan->tile_n == 128) ||
                                                  (plan->tile_m == 128 && plan->tile_n == 64) ||
                                                  (plan->tile_m == 64 && plan->tile_n == 64))) ||
-                         (plan->kgroups == 4 && plan->tile_m == 64 && plan->tile_n == 64);
+                         (plan->kgroups == 4 && plan->tile_m == 64 && plan->tile_n == 64) ||
+                         (plan->kgroups == 2 && plan->tile_m == 128 && plan->tile_n == 64);
     if (!tile_ok)
         return fail(PAM_ERROR_INVALID_VALUE,
-                    "(tile_m, tile_n, kgroups) must be (128,128,1), (128,64,1), (64,64,1) or (64,64,4)");
+                    "(tile_m, tile_n, kgroups) must be (128,128,1), (128,64,1), (128,64,2), (64,64,1) or "
+                    "(64,64,4)");
     if (plan->splits < 1 || plan->splits > kMaxSplits)
         return fail(PAM_ERROR_INVALID_VALUE, "splits must be in [1, 64]");
     if (plan->whole_tiles < 0)

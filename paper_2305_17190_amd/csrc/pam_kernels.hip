@@ -550,6 +550,8 @@ static hipError_t launch_shape(int tile_m, int tile_n, int kgroups, bool trans_a
         return launch_tile<64, 64, 1, T>(trans_a, trans_b, p, grid, stream);
     if (tile_m == 64 && tile_n == 64 && kgroups == 4)
         return launch_tile<64, 64, 4, T>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 128 && tile_n == 64 && kgroups == 2)
+        return launch_tile<128, 64, 2, T>(trans_a, trans_b, p, grid, stream);
     return hipErrorInvalidValue;
 }
 

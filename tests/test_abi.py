@@ -119,7 +119,7 @@ def test_plan_selection_is_host_logic(lib):
     assert (tm, tn) != (128, 128) and (s > 1 or kg > 1)
     for m, n, k, b in ((1, 1, 1, 1), (5, 7, 3, 1), (300, 1, 17, 1), (16, 16, 100000, 1), (64, 64, 0, 3)):
         tm, tn, s, kg, whole = pam.plan(m, n, k, b)
-        assert (tm, tn, kg) in ((128, 128, 1), (128, 64, 1), (64, 64, 1), (64, 64, 4))
+        assert (tm, tn, kg) in ((128, 128, 1), (128, 64, 1), (128, 64, 2), (64, 64, 1), (64, 64, 4))
         assert 1 <= s <= 64 and whole >= 0
     with pytest.raises(pam.PamError):
         pam.plan(0, 4, 4)

@@ -13,7 +13,7 @@ from oracle import pam_ref
 
 pytestmark = pytest.mark.gpu
 
-TILES = [(128, 128, 1), (128, 64, 1), (64, 64, 1), (64, 64, 4)]
+TILES = [(128, 128, 1), (128, 64, 1), (128, 64, 2), (64, 64, 1), (64, 64, 4)]
 CASES = 120
 
 

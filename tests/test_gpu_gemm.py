@@ -15,10 +15,11 @@ from oracle import pam_ref
 
 pytestmark = pytest.mark.gpu
 
-PLANS = [(128, 128, 1), (128, 64, 1), (64, 64, 1), (64, 64, 1, 4), (128, 128, 3), (128, 64, 7), (64, 64, 2),
-         (64, 64, 3, 4),
+PLANS = [(128, 128, 1), (128, 64, 1), (128, 64, 1, 2), (64, 64, 1), (64, 64, 1, 4), (128, 128, 3), (128, 64, 7),
+         (128, 64, 3, 2), (64, 64, 2), (64, 64, 3, 4),
          # whole-K tiles beside split ones in one launch
-         (128, 128, 3, 1, 2), (128, 64, 7, 1, 1), (64, 64, 2, 1, 5), (64, 64, 3, 4, 7), (64, 64, 5, 1, 11)]
+         (128, 128, 3, 1, 2), (128, 64, 7, 1, 1), (128, 64, 2, 2, 3), (64, 64, 2, 1, 5), (64, 64, 3, 4, 7),
+         (64, 64, 5, 1, 11)]
 TRANS = [(False, False), (False, True), (True, False), (True, True)]
 
 
@@ -296,7 +297,8 @@ def pow2_operands(shape, seed, decoy_frac):
 
 @pytest.mark.parametrize("decoys", [(0.0, 0.0), (0.01, 0.0), (0.0, 0.01), (0.02, 0.02), (0.3, 0.3)],
                          ids=["none", "A", "B", "both", "dense"])
-@pytest.mark.parametrize("plan", [(128, 128, 1), (128, 64, 2), (64, 64, 1), (64, 64, 1, 4), (64, 64, 2, 4)],
+@pytest.mark.parametrize("plan", [(128, 128, 1), (128, 64, 2), (128, 64, 1, 2), (64, 64, 1), (64, 64, 1, 4),
+                                  (64, 64, 2, 4)],
                          ids=lambda p: "x".join(map(str, p)))
 @pytest.mark.parametrize("ta,tb", [(False, True), (True, False)], ids=["NT", "TN"])
 def test_exact_sums_underflowing_products_add_nothing(decoys, plan, ta, tb):

@@ -42,7 +42,8 @@ def planted_operands(seed):
     return a, b
 
 
-@pytest.mark.parametrize("plan", [(128, 128, 1, 1, 0), (128, 64, 1, 1, 0), (64, 64, 1, 1, 0), (64, 64, 1, 4, 0)])
+@pytest.mark.parametrize("plan", [(128, 128, 1, 1, 0), (128, 64, 1, 1, 0), (128, 64, 1, 2, 0), (64, 64, 1, 1, 0),
+                                  (64, 64, 1, 4, 0)])
 @pytest.mark.parametrize("ta,tb", [(False, False), (False, True), (True, False)])
 def test_every_two_op_step_count(ta, tb, plan):
     a, b = planted_operands(31)

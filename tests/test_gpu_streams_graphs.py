@@ -1,4 +1,5 @@
-"""The PAM products on several HIP streams at once, and inside HIP graphs.
+"""The PAM products on several HIP streams and host threads at once, and
+inside HIP graphs.
 
 The binding launches on the caller's current stream and takes split-K
 workspaces from torch's stream-ordered allocator, so products may run
@@ -133,3 +134,41 @@ def test_attention_products_in_a_hip_graph():
         assert _same_bits(s_out, want_s), f"S differs on replay {rep}"
         assert _same_bits(o_out, want_o), f"O differs on replay {rep}"
     del graph
+
+
+def test_products_from_several_host_threads():
+    # The library keeps no shared host state (its error text and device
+    # check are per thread), and ctypes releases the interpreter lock during
+    # each call, so host threads drive it concurrently, each on a stream of
+    # its own; every result must equal the single-threaded product bitwise.
+    import threading
+    import torch
+    note("gemm from 4 host threads, one stream each")
+    layers = [_layer(300 + i, tokens=2048) for i in range(4)]
+    want = [_products(*l) for l in layers]
+    torch.cuda.synchronize()
+    got = [None] * 4
+    errors = []
+
+    def work(i):
+        try:
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.default_stream())
+            with torch.cuda.stream(s):
+                for _ in range(3):
+                    got[i] = _products(*layers[i])
+            s.synchronize()
+        except Exception as e:   # reported below, on the main thread
+            errors.append((i, repr(e)))
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not any(t.is_alive() for t in threads), "a worker thread did not finish"
+    assert not errors, errors
+    torch.cuda.synchronize()
+    for i in range(4):
+        for name, g, w_ in zip(("Y", "dX", "dW"), got[i], want[i]):
+            assert _same_bits(g, w_), f"thread {i} {name}"

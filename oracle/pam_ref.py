@@ -300,10 +300,13 @@ def pam_gemm_ref(a: np.ndarray, b: np.ndarray, trans_a: bool = False, trans_b: b
         opb = opb[:, np.asarray(cols, dtype=np.int64)]
     c = np.zeros((opa.shape[0], opb.shape[1]), dtype=np.float64)
     s = np.zeros_like(c)
-    for kk in range(k):
-        term = pam_mul_ref(opa[:, kk:kk + 1], opb[kk:kk + 1, :]).astype(np.float64)
-        c += term
-        s += np.abs(term)
+    # inf terms of opposite signs make a NaN sum, as IEEE addition defines;
+    # numpy's warning about it carries no information here
+    with np.errstate(invalid="ignore"):
+        for kk in range(k):
+            term = pam_mul_ref(opa[:, kk:kk + 1], opb[kk:kk + 1, :]).astype(np.float64)
+            c += term
+            s += np.abs(term)
     return c, s
 
 

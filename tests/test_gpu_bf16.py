@@ -42,6 +42,7 @@ def widened(t16):
     (96, 64, 4096, 3, False, False, False),
     (70, 300, 50, 1, True, True, True),
     (768, 192, 12608, 1, True, False, False),
+    (256, 64, 256, 256, False, False, True),     # attention P.V shape: the two-k-group 128 x 64 tile
 ])
 def test_bf16_products(m, n, k, batch, ta, tb, kinds):
     import torch

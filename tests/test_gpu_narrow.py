@@ -73,6 +73,22 @@ def test_narrow_gemm_forms(ta, tb, bits):
     narrow_case(ta, tb, 131, 70, 97, bits, 700 + bits + 2 * ta + tb)
 
 
+def test_narrow_gemm_two_kgroup_tile():
+    # the attention P.V shape, on which the library takes the two-k-group
+    # 128 x 64 tile; all 256 products against the C oracle
+    m, n, k, batch, bits = 256, 64, 256, 256, 7
+    assert pam.plan(m, n, k, batch)[::3] == (128, 2)
+    g = np.random.default_rng(712)
+    a = g.standard_normal((batch, m, k)).astype(np.float32)
+    b = (g.standard_normal((batch, k, n)) * 0.05).astype(np.float32)
+    note(f"narrow bmm on the two-k-group tile m={m} n={n} k={k} batch={batch} bits={bits}")
+    c = pam.bmm(to_dev(a), to_dev(b), mantissa_bits=bits).cpu().numpy()
+    ra, rb = pam_ref.round_mantissa_ref(a, bits), pam_ref.round_mantissa_ref(b, bits)
+    c_ref, s_ref = oracle_gemm(ra.ravel(), rb.ravel(), False, False, m, n, k, k, n, m * k, k * n,
+                               batches=list(range(batch)))
+    check_gemm(c, c_ref, s_ref, k, "narrow two-k-group tile")
+
+
 def test_narrow_gemm_batched_small_tiles_and_split():
     narrow_case(False, False, 64, 48, 300, 4, 710, batch=5)            # narrow batched outputs
     narrow_case(True, False, 96, 80, 2000, 7, 711)                     # long K: split-K

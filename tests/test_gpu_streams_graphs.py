@@ -172,3 +172,44 @@ def test_products_from_several_host_threads():
     for i in range(4):
         for name, g, w_ in zip(("Y", "dX", "dW"), got[i], want[i]):
             assert _same_bits(g, w_), f"thread {i} {name}"
+
+
+def test_bfloat16_and_narrow_products_in_a_hip_graph():
+    import torch
+    note("bfloat16 and 7-bit-mantissa products (one split-K) captured in a HIP graph, 3 replays")
+    g = np.random.default_rng(105)
+    x = to_dev(g.standard_normal((4096, 256)).astype(np.float32))
+    w = to_dev((g.standard_normal((192, 256)) * 0.05).astype(np.float32))
+    dy = to_dev((g.standard_normal((4096, 192)) * 1e-3).astype(np.float32))
+    x16, w16 = x.to(torch.bfloat16), w.to(torch.bfloat16)
+    outs = (torch.empty((4096, 192), device=device()), torch.empty((192, 256), device=device()))
+    assert pam.plan(192, 256, 4096)[2] > 1
+
+    def run():
+        pam.gemm(x16, w16, trans_b=True, out=outs[0])                       # bfloat16 operands
+        pam.gemm(dy, x, trans_a=True, out=outs[1], mantissa_bits=7)         # narrow, split-K dW
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        x.mul_(1.25)
+        x16.copy_(x.to(torch.bfloat16))
+        dy.add_(1e-4)
+        for o in outs:
+            o.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        want = (pam.gemm(x16, w16, trans_b=True), pam.gemm(dy, x, trans_a=True, mantissa_bits=7))
+        torch.cuda.synchronize()
+        for name, o, w_ in zip(("bf16 Y", "narrow dW"), outs, want):
+            assert _same_bits(o, w_), f"{name} differs on replay {rep}"
+    del graph

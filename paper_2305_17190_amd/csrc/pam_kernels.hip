@@ -395,8 +395,48 @@ pam_gemm_kernel(GemmParams p) {
         const uint32_t s2_bits = special ? 0u : (low & ~(low >> 16) & 0xFFFFu);
         const uint32_t s3_bits = special ? 0u : (low >> 16);
         const uint32_t sp_bits = special ? 0xFFFFu : 0u;
-        run_steps<BK, LDA, LDB, HM, HN, 2, -1>(s1_bits, k_first, cA, cB, ty * 4, tx * 4, acc,
-            [](float (&r)[8], uint32_t a, uint32_t, const uint32_t (&b)[8]) { s1_row(r, a, b); });
+        if constexpr (KW == 1) {
+            // All 16 steps unrolled: the reads take compile-time offsets, the
+            // next step's operands are read (unconditionally) while the
+            // current one's rows are added, and a uniform branch skips the
+            // rows of steps off the two-op path.
+            const uint32_t *a_row = &cA[2][0][ty * 4];
+            const uint32_t *b_row = &cB[0][0][tx * 4];
+            uint4 al[2], ah[2];
+            uint32_t bq[2][8];
+            auto rd = [&](int k, int slot) {
+                al[slot] = *reinterpret_cast<const uint4 *>(a_row + k * LDA);
+                ah[slot] = *reinterpret_cast<const uint4 *>(a_row + k * LDA + HM);
+                const uint4 lo = *reinterpret_cast<const uint4 *>(b_row + k * LDB);
+                const uint4 hi = *reinterpret_cast<const uint4 *>(b_row + k * LDB + HN);
+                bq[slot][0] = lo.x; bq[slot][1] = lo.y; bq[slot][2] = lo.z; bq[slot][3] = lo.w;
+                bq[slot][4] = hi.x; bq[slot][5] = hi.y; bq[slot][6] = hi.z; bq[slot][7] = hi.w;
+            };
+            if (s1_bits != 0u) {
+                rd(0, 0);
+#pragma unroll
+                for (int k = 0; k < 16; ++k) {
+                    const int cur = k & 1;
+                    if (k + 1 < 16)
+                        rd(k + 1, cur ^ 1);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if ((s1_bits >> k) & 1u) {
+                        s1_row(acc[0], al[cur].x, bq[cur]);
+                        s1_row(acc[1], al[cur].y, bq[cur]);
+                        s1_row(acc[2], al[cur].z, bq[cur]);
+                        s1_row(acc[3], al[cur].w, bq[cur]);
+                        s1_row(acc[4], ah[cur].x, bq[cur]);
+                        s1_row(acc[5], ah[cur].y, bq[cur]);
+                        s1_row(acc[6], ah[cur].z, bq[cur]);
+                        s1_row(acc[7], ah[cur].w, bq[cur]);
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+        } else {
+            run_steps<BK, LDA, LDB, HM, HN, 2, -1>(s1_bits, k_first, cA, cB, ty * 4, tx * 4, acc,
+                [](float (&r)[8], uint32_t a, uint32_t, const uint32_t (&b)[8]) { s1_row(r, a, b); });
+        }
         for (uint32_t todo = s2_bits; todo != 0u; todo &= todo - 1u) {
             const int kk = k_first + __builtin_ctz(todo);
             uint32_t am[8], mm[8], bb[8];

@@ -161,78 +161,6 @@ __device__ __forceinline__ void s3_row(float (&acc)[8], uint32_t am, uint32_t m,
 }
 
 
-// The wave's k steps in `todo` (bit k: chunk step k_first + k), each adding
-// one step of PAM products into the 8 x 8 micro-tile: `row(acc row, A value
-// of plane P0, A value of plane P1 (unused when P1 < 0), B fragment)`.
-// Software-pipelined in pairs of steps: while a step's rows are added, the
-// next step's B fragment is read into the other register set, and each half
-// of the A fragment is re-read for the next step as soon as its rows are
-// done; with an odd count one step goes first, alone.  The scheduling
-// barriers keep the compiler from moving the reads back next to their uses.
-template <int BK, int LDA, int LDB, int HM, int HN, int P0, int P1, typename Row>
-__device__ __forceinline__ void run_steps(uint32_t todo, int k_first, const uint32_t (*cA)[BK][LDA],
-                                          const uint32_t (*cB)[BK][LDB], int ra, int cb, float (&acc)[8][8],
-                                          Row row) {
-    constexpr bool kTwo = P1 >= 0;
-    auto read_a = [&](int k, int half, uint4 &x0, uint4 &x1) {
-        x0 = *reinterpret_cast<const uint4 *>(&cA[P0][k][half * HM + ra]);
-        if constexpr (kTwo)
-            x1 = *reinterpret_cast<const uint4 *>(&cA[P1 < 0 ? 0 : P1][k][half * HM + ra]);
-    };
-    auto rows = [&](int half, const uint4 &x0, const uint4 &x1, const uint32_t (&b)[8]) {
-        row(acc[4 * half + 0], x0.x, x1.x, b);
-        row(acc[4 * half + 1], x0.y, x1.y, b);
-        row(acc[4 * half + 2], x0.z, x1.z, b);
-        row(acc[4 * half + 3], x0.w, x1.w, b);
-    };
-    uint4 l0 = {}, l1 = {}, h0 = {}, h1 = {};
-    if (__builtin_popcount(todo) & 1) {
-        const int kk = k_first + __builtin_ctz(todo);
-        uint32_t bb[8];
-        lds_frag<BK, LDB>(cB, 0, kk, cb, HN, bb);
-        read_a(kk, 0, l0, l1);
-        read_a(kk, 1, h0, h1);
-        rows(0, l0, l1, bb);
-        rows(1, h0, h1, bb);
-        todo &= todo - 1u;
-    }
-    if (todo == 0u)
-        return;
-    int kk = k_first + __builtin_ctz(todo);
-    uint32_t b0[8], b1[8];
-    lds_frag<BK, LDB>(cB, 0, kk, cb, HN, b0);
-    read_a(kk, 0, l0, l1);
-    read_a(kk, 1, h0, h1);
-    auto step = [&](const uint32_t (&cur)[8], uint32_t (&nxt)[8], int kn) {
-        lds_frag<BK, LDB>(cB, 0, kn, cb, HN, nxt);
-        __builtin_amdgcn_sched_barrier(0);
-        rows(0, l0, l1, cur);
-        __builtin_amdgcn_sched_barrier(0);
-        read_a(kn, 0, l0, l1);
-        __builtin_amdgcn_sched_barrier(0);
-        rows(1, h0, h1, cur);
-        __builtin_amdgcn_sched_barrier(0);
-        read_a(kn, 1, h0, h1);
-        __builtin_amdgcn_sched_barrier(0);
-    };
-    do {
-        todo &= todo - 1u;   // an even count: a second step remains
-        const int k2 = k_first + __builtin_ctz(todo);
-        step(b0, b1, k2);
-        todo &= todo - 1u;
-        kk = todo != 0u ? k_first + __builtin_ctz(todo) : k2;   // past the last step: a harmless re-read
-        step(b1, b0, kk);
-    } while (todo != 0u);
-    // A use of the last (unneeded) reads after the loop keeps the compiler
-    // from folding the loop-carried reads into reads at the top of each
-    // iteration.
-    asm volatile("" ::"v"(b0[0]), "v"(b0[1]), "v"(b0[2]), "v"(b0[3]), "v"(b0[4]), "v"(b0[5]), "v"(b0[6]),
-                 "v"(b0[7]), "v"(l0.x), "v"(l0.y), "v"(l0.z), "v"(l0.w), "v"(h0.x), "v"(h0.y), "v"(h0.z),
-                 "v"(h0.w));
-    if constexpr (kTwo)
-        asm volatile("" ::"v"(l1.x), "v"(l1.y), "v"(l1.z), "v"(l1.w), "v"(h1.x), "v"(h1.y), "v"(h1.z), "v"(h1.w));
-}
-
 // Waves each SIMD holds for a tile shape (the register budget per wave is
 // 512 / waves): three for the 128 x 128 tile, whose loop fits 168 registers;
 // two for the smaller tiles, which stage more operand registers per thread.
@@ -387,21 +315,21 @@ pam_gemm_kernel(GemmParams p) {
         // denormals among them, no tiny normals), S3 steps (tiny normals),
         // and for a SPECIAL chunk every step with the complete definition.
         // Loops in sequence, rather than alternative paths, keep the
-        // accumulator tile in one set of registers.  The S1 loop, which takes
-        // most steps, is software-pipelined; the rarer S2 / S3 steps read
-        // their operands at the start of each step (pipelining them measured
-        // no faster).
+        // accumulator tile in one set of registers.  The S1 steps, most of
+        // them, are unrolled with the next step's reads issued ahead; the
+        // rarer S2 / S3 steps read their operands at the start of each step
+        // (reading ahead there measured no faster).
         const uint32_t s1_bits = special ? 0u : (~low & 0xFFFFu);
         const uint32_t s2_bits = special ? 0u : (low & ~(low >> 16) & 0xFFFFu);
         const uint32_t s3_bits = special ? 0u : (low >> 16);
         const uint32_t sp_bits = special ? 0xFFFFu : 0u;
-        if constexpr (KW == 1) {
-            // All 16 steps unrolled: the reads take compile-time offsets, the
-            // next step's operands are read (unconditionally) while the
-            // current one's rows are added, and a uniform branch skips the
-            // rows of steps off the two-op path.
-            const uint32_t *a_row = &cA[2][0][ty * 4];
-            const uint32_t *b_row = &cB[0][0][tx * 4];
+        {
+            // All 16 steps unrolled: the reads take compile-time offsets from
+            // the wave's k-group, the next step's operands are read
+            // (unconditionally) while the current one's rows are added, and a
+            // uniform branch skips the rows of steps off the two-op path.
+            const uint32_t *a_row = &cA[2][k_first][ty * 4];
+            const uint32_t *b_row = &cB[0][k_first][tx * 4];
             uint4 al[2], ah[2];
             uint32_t bq[2][8];
             auto rd = [&](int k, int slot) {
@@ -433,9 +361,6 @@ pam_gemm_kernel(GemmParams p) {
                     __builtin_amdgcn_sched_barrier(0);
                 }
             }
-        } else {
-            run_steps<BK, LDA, LDB, HM, HN, 2, -1>(s1_bits, k_first, cA, cB, ty * 4, tx * 4, acc,
-                [](float (&r)[8], uint32_t a, uint32_t, const uint32_t (&b)[8]) { s1_row(r, a, b); });
         }
         for (uint32_t todo = s2_bits; todo != 0u; todo &= todo - 1u) {
             const int kk = k_first + __builtin_ctz(todo);

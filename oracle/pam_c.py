@@ -19,12 +19,15 @@ _lib = None
 
 
 def build(verbose: bool = False) -> str:
-    """Compile the C oracle with gcc -O2 (no fast-math) and OpenMP."""
-    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-o", LIB + ".tmp", SRC, "-lm"]
+    """Compile the C oracle with gcc -O2 (no fast-math) and OpenMP.  The
+    library is written under a per-process name and renamed into place, so
+    concurrent builds (parallel test workers) never see a partial file."""
+    tmp = f"{LIB}.{os.getpid()}.tmp"
+    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-o", tmp, SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(tmp, LIB)
     return LIB
 
 

@@ -40,15 +40,16 @@ def sources():
 
 
 def build(verbose: bool = False, extra_flags=()) -> str:
+    tmp = f"{LIB}.{os.getpid()}.tmp"   # per process: concurrent builds never see a partial file
     cmd = [hipcc(), *DEVICE_FLAGS, *extra_flags, "-fPIC", "-shared", "-I", INCLUDE, "-I", CSRC,
-           *sources(), "-o", LIB + ".tmp", "-lhsa-runtime64"]
+           *sources(), "-o", tmp, "-lhsa-runtime64"]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError("hipcc failed to build libpam.so")
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(tmp, LIB)
     return LIB
 
 

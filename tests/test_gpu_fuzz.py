@@ -3,7 +3,10 @@ oracle: random sizes (ragged in every dimension), transposes, batch counts,
 padded leading dimensions and batch strides, every tile shape, random split
 counts and whole-tile counts (hybrid plans), plus the library's own plan;
 then the same with narrow-mantissa and bfloat16 operands.  Each case is
-compared element by element within the GEMM tolerance."""
+compared element by element within the GEMM tolerance.  The environment
+variable PAM_FUZZ_CASES sets the number of cases of the first sweep."""
+import os
+
 import numpy as np
 import pytest
 
@@ -14,7 +17,8 @@ from oracle import pam_ref
 pytestmark = pytest.mark.gpu
 
 TILES = [(128, 128, 1), (128, 64, 1), (128, 64, 2), (64, 64, 1), (64, 64, 4)]
-CASES = 120
+# PAM_FUZZ_CASES widens the sweep (same seeds first, then new ones).
+CASES = int(os.environ.get("PAM_FUZZ_CASES", "1000"))
 
 
 def draw(rng):
@@ -68,7 +72,7 @@ def test_random_products(case):
     check_gemm(got[:, :, :n], c_ref, s_ref, k, f"fuzz {case}")
 
 
-NARROW_CASES = 40
+NARROW_CASES = 200
 
 
 @pytest.mark.parametrize("case", range(NARROW_CASES))

@@ -60,7 +60,7 @@ struct Shape {
 // three waves per SIMD, the others two.
 const Shape kShapes[] = {{128, 128, 1, 4, 3, 26.67e12},
                          {128, 64, 1, 2, 4, 20.49e12},
-                         {128, 64, 2, 4, 2, 19.6e12},
+                         {128, 64, 2, 4, 2, 20.6e12},
                          {64, 64, 1, 1, 8, 19.64e12},
                          {64, 64, 4, 4, 2, 15.99e12}};
 constexpr int kComputeUnits = 256;

@@ -2,7 +2,8 @@
 oracle: random sizes (ragged in every dimension), transposes, batch counts,
 padded leading dimensions and batch strides, every tile shape, random split
 counts and whole-tile counts (hybrid plans), plus the library's own plan;
-then the same with narrow-mantissa and bfloat16 operands.  Each case is
+large outputs whose whole-K tiles span several rounds of resident
+workgroups; then the same with narrow-mantissa and bfloat16 operands.  Each case is
 compared element by element within the GEMM tolerance.  The environment
 variable PAM_FUZZ_CASES sets the number of cases of the first sweep."""
 import os
@@ -70,6 +71,49 @@ def test_random_products(case):
     assert np.all(np.isnan(got[:, :, n:])), "wrote outside the output's columns"
     c_ref, s_ref = oracle_gemm(a_buf, b_buf, ta, tb, m, n, k, lda, ldb, sa, sb, batches=list(range(batch)))
     check_gemm(got[:, :, :n], c_ref, s_ref, k, f"fuzz {case}")
+
+
+# Resident workgroups of each tile shape on the 256 compute units.
+SLOTS = {(128, 128, 1): 768, (128, 64, 1): 1024, (128, 64, 2): 512, (64, 64, 1): 2048, (64, 64, 4): 512}
+LARGE_CASES = 30
+
+
+@pytest.mark.parametrize("case", range(LARGE_CASES))
+def test_random_large_products(case):
+    # Outputs of 1000-4200 square, more tiles than resident workgroups, so
+    # whole-K tiles span several rounds before the split ones (hybrid plans
+    # whose whole-tile count is a multiple of the resident slots, as the
+    # library plans them, or any count).  Compared in full with the C oracle.
+    rng = np.random.default_rng(9000 + case)
+    m, n = (int(x) for x in rng.integers(1000, 4200, size=2))
+    k = int(rng.integers(16, 520))
+    ta, tb = bool(rng.integers(0, 2)), bool(rng.integers(0, 2))
+    tm, tn, kg = TILES[case % len(TILES)]
+    tiles = -(-m // tm) * -(-n // tn)
+    splits = int(rng.integers(1, 9))
+    slots = SLOTS[(tm, tn, kg)]
+    if case % 2 == 0 and tiles > slots:
+        whole = slots * int(rng.integers(1, tiles // slots + 1))
+        whole = min(whole, tiles - 1)
+    else:
+        whole = int(rng.integers(0, tiles + 1))
+    plan = (tm, tn, splits, kg, whole)
+    a_rows, a_cols = (k, m) if ta else (m, k)
+    b_rows, b_cols = (n, k) if tb else (k, n)
+    a_buf = rng.standard_normal(a_rows * a_cols).astype(np.float32)
+    b_buf = rng.standard_normal(b_rows * b_cols).astype(np.float32)
+    if case % 3 == 0:                                      # zeros, denormals and tiny values
+        for buf in (a_buf, b_buf):
+            idx = rng.choice(buf.size, size=max(1, buf.size // 500), replace=False)
+            buf[idx[0::3]] = 0.0
+            buf[idx[1::3]] = np.float32(3e-41)
+            buf[idx[2::3]] = np.float32(1.5e-38)
+    note(f"fuzz large {case}: m={m} n={n} k={k} ta={ta} tb={tb} plan={plan} tiles={tiles}")
+    da = to_dev(a_buf).view(1, a_rows, a_cols)
+    db = to_dev(b_buf).view(1, b_rows, b_cols)
+    got = pam.bmm(da, db, trans_a=ta, trans_b=tb, plan=plan).cpu().numpy()
+    c_ref, s_ref = oracle_gemm(a_buf, b_buf, ta, tb, m, n, k, a_cols, b_cols, batches=[0])
+    check_gemm(got, c_ref, s_ref, k, f"fuzz large {case}")
 
 
 NARROW_CASES = 200

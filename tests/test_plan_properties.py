@@ -42,3 +42,27 @@ def test_plans_are_valid(m, n, k, batch):
         per_launch = max(1, 16777215 // ((tiles // batch) * splits))
         split_tiles = min(batch, per_launch) * (tiles // batch)
     assert size.value == splits * split_tiles * tm * tn * 4
+
+
+# The plans the library picks for the benchmark products (tile_m, tile_n,
+# splits, k-groups, whole-K tiles), each measured within a few per cent of the
+# fastest plan of an exhaustive sweep: a change of the cost model that moves
+# one of them has to be measured again.
+WORKLOAD_PLANS = {
+    (2, "fwd"): (128, 128, 1, 1, 0), (2, "dX"): (128, 64, 3, 1, 0), (2, "dW"): (128, 128, 61, 1, 0),
+    (3, "up"): (128, 128, 2, 1, 768), (3, "down"): (128, 128, 8, 1, 0), (3, "dH"): (128, 128, 2, 1, 768),
+    (3, "dW2"): (128, 128, 32, 1, 0), (3, "dX"): (128, 128, 8, 1, 0), (3, "dW1"): (128, 128, 32, 1, 0),
+    (4, "QKt"): (128, 128, 1, 1, 0), (4, "PV"): (128, 64, 1, 2, 0), (4, "dP"): (128, 128, 1, 1, 0),
+    (4, "dV"): (128, 64, 1, 2, 0), (4, "dQ"): (128, 64, 1, 2, 0), (4, "dK"): (128, 64, 1, 2, 0),
+    (5, "fwd"): (128, 128, 8, 1, 3840), (5, "dX"): (128, 128, 8, 1, 3840), (5, "dW"): (128, 128, 8, 1, 768),
+}
+
+
+def test_workload_plans_are_pinned():
+    import pam_workloads as wl
+    seen = set()
+    for w in (2, 3, 4, 5):
+        for f in wl.WORKLOADS[w]["forms"]:
+            assert pam.plan(f.m, f.n, f.k, f.batch) == WORKLOAD_PLANS[(w, f.name)], (w, f.name)
+            seen.add((w, f.name))
+    assert seen == set(WORKLOAD_PLANS)

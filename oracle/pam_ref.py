@@ -51,19 +51,34 @@ in the HIP library):
       float format's conversion does; inf stays inf and NaN stays NaN.  The
       rounded inputs then go through PAM (R1-R7) with float32 accumulation.
 
-  R15 exact derivative (Table 1: d(A .^ B)/dA = 2^(E_B + 1{M_A + M_B >= 1})):
-      the sign of B is part of it (d(A .^ B)/dA = sgn(B) 2^(E_B + c) for
-      either sign of A, since the magnitude of A .^ B grows with |A| and its
-      sign is S_A + S_B); a zero or denormal A or B gives 0 (A .^ B is
-      identically zero around a zero / denormal B, and flushed to zero
-      around a zero A).  The formula is applied for all normal A, B, also
-      where A .^ B itself under- or overflows.  For a matrix product
-      Y = X .^ W^T the exact derivatives are
+  R15 exact derivative (Table 1: d(A .^ B)/dA = 2^(E_B + 1{M_A + M_B >= 1})
+      with no sign and no edge cases; Sec. "Derivatives": the exact
+      derivative is the true, piecewise constant derivative of the piecewise
+      affine function):
+      * the sign of B is part of it: d(A .^ B)/dA = sgn(B) 2^(E_B + c) for
+        either sign of A, since the magnitude of A .^ B grows with |A| and its
+        sign is S_A + S_B;
+      * it is 0 wherever A .^ B is clamped to a constant: a zero or denormal A
+        or B (R2, R3), a result that underflows to a signed zero (R4: the
+        magnitude sum |A| + |B| - bias below 0x00800000) and a result that
+        saturates at +-FLT_MAX (R5: that sum above 0x7F7FFFFF) -- the function
+        is flat there, so its true derivative is zero;
+      * elsewhere (the sum in [0x00800000, 0x7F7FFFFF], the result not
+        clamped) it is Table 1's power of two.  That is the slope of the
+        affine piece A .^ B follows as |A| grows from A (where the carry
+        flips, 1{M_A + M_B >= 1} takes the upper piece); at a sum of exactly
+        0x7F7FFFFF, the unclamped FLT_MAX itself, the slope of the piece below
+        (e.g. d(A .^ 1)/dA = 1 for every normal A, FLT_MAX included).
+      For a matrix product Y = X .^ W^T the exact derivatives are
         dX[i,k] = sum_j dY[i,j] d(X[i,k] .^ W[j,k])/dX[i,k]
-        dW[j,k] = sum_i dY[i,j] d(W[j,k] .^ X[i,k])/dW[j,k],
-      the terms exact (a power of two times dY; a denormal dY counts as
-      zero, as R3), accumulated in float32.  Inf / NaN operands are outside
-      this reading (parity unpinned there).
+        dW[j,k] = sum_i dY[i,j] d(W[j,k] .^ X[i,k])/dW[j,k].
+      Each term dY * g with g a power of two is exact (Sec. "Derivatives":
+      such a product is performed exactly by PAM), and PAM reads a denormal
+      operand as zero (R3), so a denormal dY contributes nothing; the terms
+      are accumulated in float32 (here: float64, plus S = sum |terms|).
+      A term whose exact value leaves the float32 range is kept exact here;
+      the float32 sum rounds it like any other addend.  Inf / NaN operands
+      are outside this reading (parity unpinned there).
 
 Three independent renderings of the scalar product are given (bit, field and
 value form); the tests check them against each other and against the facts
@@ -323,7 +338,11 @@ def pam_gemm_batched_ref(a: np.ndarray, b: np.ndarray, trans_a: bool = False, tr
 
 
 def pam_exact_grad_factor(a: np.ndarray, b: np.ndarray) -> np.ndarray:
-    """d(a .^ b)/da in float64 (Table 1, reading R15), elementwise, broadcasting."""
+    """d(a .^ b)/da in float64 (Table 1, reading R15), elementwise, broadcasting.
+
+    sgn(b) 2^(E_b + 1{M_a + M_b >= 1}) where a .^ b is not clamped, 0 where it
+    is (zero / denormal operand, underflow, saturation).  Finite operands only.
+    """
     a = np.asarray(a, dtype=np.float32)
     b = np.asarray(b, dtype=np.float32)
     ua = a.view(np.uint32).astype(np.int64)
@@ -333,14 +352,17 @@ def pam_exact_grad_factor(a: np.ndarray, b: np.ndarray) -> np.ndarray:
     carry = ((fa + fb) >= (1 << 23)).astype(np.int64)          # 1{M_A + M_B >= 1}
     sign = np.where(ub >> 31 == 1, -1.0, 1.0)
     g = sign * np.ldexp(1.0, (eb - 127 + carry).astype(np.int64))
-    return np.where((ea == 0) | (eb == 0), 0.0, g)
+    t = (ua & MAG) + (ub & MAG) - BIAS                         # magnitude of a .^ b before R4 / R5
+    flat = (ea == 0) | (eb == 0) | (t < MIN_NORMAL) | (t > FLT_MAX)
+    return np.where(flat, 0.0, g)
 
 
 def pam_exact_grads_ref(dy: np.ndarray, x: np.ndarray, w: np.ndarray):
     """Exact derivatives of Y = X .^ W^T (Table 1, R15): (dX, S_dX, dW, S_dW)
     in float64, S = sum of |terms|.  dy [T, N], x [T, K], w [N, K]."""
     dy = np.asarray(dy, dtype=np.float32)
-    dy = np.where(np.abs(dy) < np.float32(2.0 ** -126), np.float32(0.0), dy).astype(np.float64)   # denormal dY as zero
+    # a denormal dY is a zero operand of the term's PAM (R3)
+    dy = np.where(np.abs(dy) < np.float32(2.0 ** -126), np.float32(0.0), dy).astype(np.float64)
     t, n = dy.shape
     k = np.asarray(x).shape[1]
     dx = np.zeros((t, k))

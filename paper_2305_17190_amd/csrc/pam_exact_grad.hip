@@ -1,29 +1,43 @@
 // Exact-derivative PAM products on gfx950 (Kosson & Jaggi, Table 1).
 //
-// The exact derivative of A .^ B with respect to A is sgn(B) 2^(E_B + c),
-// c = 1{M_A + M_B >= 1}: a power of two, so each backward term is exact.  For
-// Y = X .^ W^T the two gradients are contractions in which every term also
-// depends on an output-shaped operand through the carry c:
+// The exact derivative of A .^ B with respect to A is the slope of the
+// piecewise affine function: sgn(B) 2^(E_B + c), c = 1{M_A + M_B >= 1}, where
+// A .^ B is not clamped, and 0 where it is (a zero or denormal operand, a
+// result that underflows to a signed zero or saturates at +-FLT_MAX): the
+// function is constant there.  For Y = X .^ W^T the two gradients are
+// contractions in which every term also depends on an output-shaped operand:
 //
 //   dX[i,k] = sum_j dY[i,j] d(X[i,k] .^ W[j,k]) / dX[i,k]
 //   dW[j,k] = sum_i dY[i,j] d(W[j,k] .^ X[i,k]) / dW[j,k]
 //
-// Both are C(r, c) = sum_q op(A)(r, q) g(B(q, c), Mod(r, c)) with
-// g(b, mod) = sgn(b) 2^(E_b + 1{M_b + M_mod >= 1}) (zero when b or mod is zero
-// or denormal): dX is (A = dY, B = W, Mod = X), dW is (A = dY^T, B = X,
-// Mod = W).
+// Both are C(r, c) = sum_q op(A)(r, q) g(B(q, c), Mod(r, c)) with g(b, mod) =
+// d(mod .^ b) / d mod: dX is (A = dY, B = W, Mod = X), dW is (A = dY^T,
+// B = X, Mod = W).  Each term A * g is exact (g is a power of two) and added
+// with one rounding (fma); a denormal A counts as zero.
 //
-// Per term, with b's encoding staged in LDS (zero and denormal b as 0) and
-// mod's mantissa field held in a register per output: t = b + M_mod (one
-// int add) carries into b's exponent exactly when M_b + M_mod >= 1, and
-// clearing t's mantissa (one and) leaves the float sgn(b) 2^(E_b + c); then
-// one fma adds dY * g.  Three full-rate vector ops per term; the product dY *
-// g is exact, and the fma adds it unrounded.  Outputs whose Mod is zero or
-// denormal are zero.
+// Fast path.  Call a normal value "safe" when its exponent field is in
+// [64, 190].  For safe b and safe mod the product mod .^ b can never leave the
+// normal range and 2^(E_b + c) <= 2^64, so per term: t = b + M_mod (one int
+// add: it carries into b's exponent exactly when M_b + M_mod >= 1), clearing
+// t's mantissa (one and) leaves the float sgn(b) 2^(E_b + c), and one fma adds
+// A * g.  Zero and denormal b are staged as 0, which gives g = 0.
 //
-// Tiling follows the PAM matrix product: 128 x 128 output tile per 256-thread
-// workgroup, 8 x 8 register micro-tiles, K in LDS chunks of 16; split-K into
-// the workspace p.W when several K slices run.
+// The rest, taken by the complete definition (general_fma):
+//   * b that is normal but not safe ("extreme"): staged as 0 for the fast
+//     path, and the LDS chunk's steps holding one are flagged; in a flagged
+//     step each thread adds the general term for its columns whose b is
+//     extreme.
+//   * mod that is normal but not safe: the output's fast-path sum is
+//     discarded; up to two such outputs per thread keep their own
+//     accumulator, summed over every k with the general term.  A workgroup
+//     with a thread holding more takes the general term for every term.
+//   * zero / denormal mod: the output is zero.
+// The general term needs mod's exponent field, kept for the whole tile in
+// LDS as bytes; mod's mantissa stays in registers for the fast path.
+//
+// Tiling: 128 x 128 output tile per 256-thread workgroup, 8 x 8 register
+// micro-tiles, K in LDS chunks of 16; split-K into the workspace p.W when
+// several K slices run.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -34,20 +48,40 @@
 namespace pamk {
 namespace {
 
-// Raw operand words into one k-major LDS plane s[kk][o]; with `flush`, zero
-// and denormal words become +0 (the B side: such a b has a zero factor).
+constexpr uint32_t kSafeLo = 64u;    // exponent fields [64, 190]: the fast path is exact
+constexpr uint32_t kSafeHi = 190u;
+
+// Normal (field 1..254; inf / NaN count too) but outside the safe band.
+__device__ __forceinline__ bool extreme(uint32_t u) {
+    const uint32_t f = (u >> 23) & 0xFFu;
+    return f != 0u && (f < kSafeLo || f > kSafeHi);
+}
+
+// acc += a * d(mod .^ b)/d mod, the complete definition for finite operands:
+// zero when b or mod is zero / denormal or mod .^ b is clamped (magnitude sum
+// |b| + |mod| - bias outside [2^-126's, FLT_MAX's encoding]); otherwise
+// sgn(b) 2^(E_b + c).  2^128 (E_b = 127 with the carry) is applied as
+// (2a) * 2^127 (exact: a doubling).
+__device__ __forceinline__ void general_fma(float &acc, float a, uint32_t b, uint32_t mod) {
+    const uint32_t mb = b & kMag;
+    const uint32_t md = mod & kMag;
+    const uint32_t sum = mb + md;   // < 2^32: both magnitudes are below 2^31
+    const bool live = mb >= kMinNormal && md >= kMinNormal && sum >= kBias + kMinNormal && sum <= kBias + kFltMax;
+    uint32_t g = (b + (md & kMant)) & kSignExp;
+    const bool top = (g & kExpMask) == kExpMask;
+    g = top ? g - (1u << 23) : g;
+    const float a2 = top ? a * 2.0f : a;
+    g = live ? g : 0u;
+    acc = fmaf(a2, __uint_as_float(g), acc);
+}
+
+// Raw operand words into one k-major LDS plane s[kk][o].
 template <int LDS_LD, int D, int NT, int BK, bool KCONTIG>
-__device__ __forceinline__ void store_plane(const TileLoader<D, NT, BK, KCONTIG> &ld, uint32_t (*s)[LDS_LD],
-                                            int tid, bool flush) {
+__device__ __forceinline__ void store_a(const TileLoader<D, NT, BK, KCONTIG> &ld, uint32_t (*s)[LDS_LD], int tid) {
     using TL = TileLoader<D, NT, BK, KCONTIG>;
 #pragma unroll
     for (int r = 0; r < TL::L; ++r) {
-        uint32_t e[4] = {ld.v[r].x, ld.v[r].y, ld.v[r].z, ld.v[r].w};
-        if (flush) {
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-                e[c] = ((e[c] & kExpMask) == 0u) ? 0u : e[c];
-        }
+        const uint32_t e[4] = {ld.v[r].x, ld.v[r].y, ld.v[r].z, ld.v[r].w};
         const int o = TL::grp_o(tid, r);
         const int kk = TL::grp_k(tid, r);
         if (KCONTIG) {
@@ -57,6 +91,37 @@ __device__ __forceinline__ void store_plane(const TileLoader<D, NT, BK, KCONTIG>
         } else {
             *reinterpret_cast<uint4 *>(&s[kk][o]) = make_uint4(e[0], e[1], e[2], e[3]);
         }
+    }
+}
+
+// B (k-major in memory, rows kk, columns o) into two planes: plane 0 for the
+// fast path (zero, denormal and extreme b as 0), plane 1 for the general
+// term (zero and denormal b as 0, extreme b kept); a chunk step holding an
+// extreme b sets its bit in *slow.
+template <int LDS_LD, int D, int NT, int BK>
+__device__ __forceinline__ void store_b(const TileLoader<D, NT, BK, false> &ld, uint32_t (*s)[BK][LDS_LD], int tid,
+                                        uint32_t *slow) {
+    using TL = TileLoader<D, NT, BK, false>;
+#pragma unroll
+    for (int r = 0; r < TL::L; ++r) {
+        const uint32_t e[4] = {ld.v[r].x, ld.v[r].y, ld.v[r].z, ld.v[r].w};
+        uint32_t fast[4], full[4];
+        bool any = false;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const uint32_t u = e[c];
+            const bool zero = (u & kExpMask) == 0u;
+            const bool ext = extreme(u);
+            full[c] = zero ? 0u : u;
+            fast[c] = (zero || ext) ? 0u : u;
+            any = any || ext;
+        }
+        const int o = TL::grp_o(tid, r);
+        const int kk = TL::grp_k(tid, r);
+        *reinterpret_cast<uint4 *>(&s[0][kk][o]) = make_uint4(fast[0], fast[1], fast[2], fast[3]);
+        *reinterpret_cast<uint4 *>(&s[1][kk][o]) = make_uint4(full[0], full[1], full[2], full[3]);
+        if (any)
+            atomicOr(slow, 1u << kk);
     }
 }
 
@@ -102,8 +167,12 @@ pam_exact_grad_kernel(GemmParams p) {
     constexpr int TXN = BN / 8;
     constexpr int HM = BM / 2, HN = BN / 2;
     constexpr int LDA = BM + 4, LDB = BN + 4;
+    constexpr int LDE = BN / 4 + 1;   // words per row of the Mod exponent bytes
     __shared__ __attribute__((aligned(16))) uint32_t sA[BK][LDA];
-    __shared__ __attribute__((aligned(16))) uint32_t sB[BK][LDB];
+    __shared__ __attribute__((aligned(16))) uint32_t sB[2][BK][LDB];
+    __shared__ uint32_t sE[BM][LDE];   // Mod exponent fields, four columns per word
+    __shared__ uint32_t sSlow[2];      // [chunk parity] steps holding an extreme b
+    __shared__ uint32_t sDense;        // some thread has more than two extreme-Mod outputs
 
     const int tid = threadIdx.x;
     const int tx = tid % TXN;
@@ -130,24 +199,56 @@ pam_exact_grad_kernel(GemmParams p) {
     la.init(p.lda, m0, p.m, tid);
     lb.init(p.ldb, n0, p.n, tid);
 
-    // The micro-tile's Mod mantissas, fixed for the whole K loop (the
-    // epilogue reads Mod again for the zero / denormal test, so no flags stay
-    // live through the loop).
+    if (tid < 2)
+        sSlow[tid] = 0u;
+    if (tid == 0)
+        sDense = 0u;
+    __syncthreads();
+
+    // The micro-tile's Mod mantissas, fixed for the whole K loop, and its
+    // exponent fields in LDS; up to two outputs with an extreme Mod keep
+    // their own accumulator (row, column and Mod word).
     uint32_t mm[8][8];
+    int nside = 0;
+    uint32_t side_rc[2] = {0u, 0u};
+    uint32_t side_mod[2] = {0u, 0u};
+    float side_acc[2] = {0.0f, 0.0f};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const int row = m0 + (i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4));
+        const int lr = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+        const int row = m0 + lr;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int col = n0 + (j < 4 ? tx * 4 + j : HN + tx * 4 + (j - 4));
-            uint32_t u = 0u;
-            if (row < p.m && col < p.n)
-                u = __float_as_uint(p.Mod[(int64_t)row * p.ldm + col]);
-            // kept as computed: re-deriving it inside the loop would cost an
-            // op per term
-            asm volatile("v_and_b32 %0, 0x7fffff, %1" : "=v"(mm[i][j]) : "v"(u));
+        for (int h = 0; h < 2; ++h) {
+            uint32_t fields = 0u;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const int j = 4 * h + jj;
+                const int lc = (h == 0 ? tx * 4 : HN + tx * 4) + jj;
+                const int col = n0 + lc;
+                uint32_t u = 0u;
+                if (row < p.m && col < p.n)
+                    u = __float_as_uint(p.Mod[(int64_t)row * p.ldm + col]);
+                // kept as computed: re-deriving it inside the loop would cost
+                // an op per term
+                asm volatile("v_and_b32 %0, 0x7fffff, %1" : "=v"(mm[i][j]) : "v"(u));
+                fields |= ((u >> 23) & 0xFFu) << (8 * jj);
+                if (extreme(u)) {
+                    const uint32_t rc = ((uint32_t)lr << 16) | (uint32_t)lc;
+                    if (nside == 0) {
+                        side_rc[0] = rc;
+                        side_mod[0] = u;
+                    } else {
+                        side_rc[1] = rc;
+                        side_mod[1] = u;
+                    }
+                    ++nside;
+                }
+            }
+            sE[lr][(h == 0 ? tx : HN / 4 + tx)] = fields;
         }
     }
+    if (nside > 2)
+        sDense = 1u;
 
     float acc[8][8];
 #pragma unroll
@@ -160,30 +261,67 @@ pam_exact_grad_kernel(GemmParams p) {
         la.load(a_base, m0, p.m, kb, ke, vec_a, tid);
         lb.load(b_base, n0, p.n, kb, ke, vec_b, tid);
     }
+    __syncthreads();
+    const bool dense = sDense != 0u;
+
     for (int c = 0; c < nchunks; ++c) {
         __syncthreads();   // every wave is done reading the previous chunk
-        store_plane<LDA>(la, sA, tid, false);
-        store_plane<LDB>(lb, sB, tid, true);
+        store_a<LDA>(la, sA, tid);
+        store_b<LDB>(lb, sB, tid, &sSlow[c & 1]);
         __syncthreads();
+        const uint32_t slow = __builtin_amdgcn_readfirstlane(sSlow[c & 1]);
+        if (tid == 0)
+            sSlow[(c + 1) & 1] = 0u;   // next chunk's flags; last read one chunk ago
         if (c + 1 < nchunks) {
             const int k0 = kb + (c + 1) * BK;
             la.load(a_base + (c + 1) * a_step, m0, p.m, k0, ke, vec_a, tid);
             lb.load(b_base + (c + 1) * b_step, n0, p.n, k0, ke, vec_b, tid);
         }
+        if (!dense) {
 #pragma unroll 1
-        for (int kk = 0; kk < BK; ++kk) {
-            uint32_t av[8], bv[8];
-            const uint4 a_lo = *reinterpret_cast<const uint4 *>(&sA[kk][ty * 4]);
-            const uint4 a_hi = *reinterpret_cast<const uint4 *>(&sA[kk][HM + ty * 4]);
-            const uint4 b_lo = *reinterpret_cast<const uint4 *>(&sB[kk][tx * 4]);
-            const uint4 b_hi = *reinterpret_cast<const uint4 *>(&sB[kk][HN + tx * 4]);
-            av[0] = a_lo.x; av[1] = a_lo.y; av[2] = a_lo.z; av[3] = a_lo.w;
-            av[4] = a_hi.x; av[5] = a_hi.y; av[6] = a_hi.z; av[7] = a_hi.w;
-            bv[0] = b_lo.x; bv[1] = b_lo.y; bv[2] = b_lo.z; bv[3] = b_lo.w;
-            bv[4] = b_hi.x; bv[5] = b_hi.y; bv[6] = b_hi.z; bv[7] = b_hi.w;
+            for (int kk = 0; kk < BK; ++kk) {
+                uint32_t av[8], bv[8];
+                lds_frag<BK, LDA>(&sA, 0, kk, ty * 4, HM, av);
+                lds_frag<BK, LDB>(sB, 0, kk, tx * 4, HN, bv);
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
-                exact_row(acc[i], __uint_as_float(av[i]), bv, mm[i]);
+                for (int i = 0; i < 8; ++i)
+                    exact_row(acc[i], __uint_as_float(av[i]), bv, mm[i]);
+            }
+        }
+        // Steps with an extreme b (every step in a dense workgroup): the
+        // general term for the columns whose b is extreme (every column).
+#pragma unroll 1
+        for (uint32_t todo = dense ? 0xFFFFu : slow; todo != 0u; todo &= todo - 1u) {
+            const int kk = __builtin_ctz(todo);
+            uint32_t av[8], bv[8];
+            lds_frag<BK, LDA>(&sA, 0, kk, ty * 4, HM, av);
+            lds_frag<BK, LDB>(sB, 1, kk, tx * 4, HN, bv);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (dense || extreme(bv[j])) {
+                    const int h = j / 4;
+                    const int sh = 8 * (j % 4);
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        const int lr = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+                        const uint32_t f = (sE[lr][(h == 0 ? tx : HN / 4 + tx)] >> sh) & 0xFFu;
+                        general_fma(acc[i][j], __uint_as_float(av[i]), bv[j], (f << 23) | mm[i][j]);
+                    }
+                }
+            }
+        }
+        // Outputs with an extreme Mod, every step.
+        if (!dense) {
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                if (e < nside) {
+                    const int lr = (int)(side_rc[e] >> 16);
+                    const int lc = (int)(side_rc[e] & 0xFFFFu);
+#pragma unroll 4
+                    for (int kk = 0; kk < BK; ++kk)
+                        general_fma(side_acc[e], __uint_as_float(sA[kk][lr]), sB[1][kk][lc], side_mod[e]);
+                }
+            }
         }
     }
 
@@ -209,6 +347,19 @@ pam_exact_grad_kernel(GemmParams p) {
             if (col < p.n) {
                 const bool zero_mod = (__float_as_uint(mrow[col]) & kExpMask) == 0u;
                 orow[col] = zero_mod ? 0.0f : acc[i][j];
+            }
+        }
+    }
+    // The extreme-Mod outputs' own sums replace what was just written (same
+    // thread, same address, later in program order).
+    if (!dense) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            if (e < nside) {
+                const int row = m0 + (int)(side_rc[e] >> 16);
+                const int col = n0 + (int)(side_rc[e] & 0xFFFFu);
+                if (row < p.m && col < p.n)
+                    out[(int64_t)row * ld + col] = side_acc[e];
             }
         }
     }

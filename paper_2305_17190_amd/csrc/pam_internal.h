@@ -67,7 +67,7 @@ hipError_t launch_split_tile_reduce(int tile_m, int tile_n, const GemmParams &p,
 constexpr int64_t kMaxLaunchItems = 16777215;
 
 // Exact-derivative product (pam_exact_grad.hip): C(r, c) = sum_q op(A)(r, q)
-// d(B(q, c) .^ Mod(r, c)) / dB(q, c); 128 x 128 tiles, grid (tiles, splits).
+// d(Mod(r, c) .^ B(q, c)) / dMod(r, c); 128 x 128 tiles, grid (tiles, splits).
 hipError_t launch_pam_exact_grad(bool trans_a, const GemmParams &p, hipStream_t stream);
 
 // Exact-derivative products: C[b][i][j] = sum_s W[b][s][i][j], s in

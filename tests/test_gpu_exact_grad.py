@@ -1,5 +1,9 @@
 """Exact-derivative products (Table 1, reading R15) on the GPU against the
-oracle, directly and through pam_linear(derivative="exact")."""
+oracle, directly and through pam_linear(derivative="exact"): ordinary
+operands, every exponent region of every operand (zero / denormal, the safe
+band, tiny and huge normals, products that underflow or saturate, the 2^128
+factor), single-term and 16-term sums compared bit for bit, workgroups with
+few and with many outputs whose X or W is tiny or huge, split K."""
 import numpy as np
 import pytest
 
@@ -24,6 +28,107 @@ def operands(t, n, k, seed, edges=False):
             flat[idx] = np.where(kinds == 0, 0.0, np.where(kinds == 1, -0.0, np.where(
                 kinds == 2, 1e-40 * s, 1.5 * 2.0 ** -120))).astype(np.float32)
     return x, w, dy
+
+
+def region_values(shape, g, lo_share=0.3, hi_share=0.3, zero_share=0.1):
+    """float32 values whose exponent fields cover every region: the band
+    [64, 190] where products cannot leave the normal range, tiny normals
+    (1..63), huge normals (191..254), zeros and denormals."""
+    u = g.random(shape)
+    field = np.where(u < lo_share, g.integers(1, 64, shape),
+                     np.where(u < lo_share + hi_share, g.integers(191, 255, shape), g.integers(64, 191, shape)))
+    mant = g.integers(0, 1 << 23, shape)
+    sign = g.integers(0, 2, shape)
+    bits = (sign << 31) | (field << 23) | mant
+    z = g.random(shape) < zero_share
+    bits = np.where(z, np.where(g.random(shape) < 0.5, sign << 31, (sign << 31) | g.integers(1, 1 << 23, shape)), bits)
+    return bits.astype(np.uint32).view(np.float32)
+
+
+def small_dy(shape, g):
+    """dY at most 2^-9 in magnitude (no term reaches FLT_MAX: factors are at
+    most 2^128), down to the tiny normals, with zeros and denormals."""
+    field = g.integers(1, 118, shape)
+    bits = (g.integers(0, 2, shape) << 31) | (field << 23) | g.integers(0, 1 << 23, shape)
+    bits = np.where(g.random(shape) < 0.05, g.integers(0, 1 << 23, shape), bits)
+    return bits.astype(np.uint32).view(np.float32)
+
+
+def check_single_terms(got, ref, what):
+    """One term per output: the kernel's fma rounds the exact term once, so a
+    normal result equals the float32 rounding of the exact value bit for bit;
+    results below 2^-126 are flushed."""
+    got = np.asarray(got, np.float32)
+    with np.errstate(over="ignore"):
+        ref32 = ref.astype(np.float32)
+    normal = np.abs(ref32) >= np.float32(2.0 ** -126)
+    assert np.array_equal(got[normal].view(np.uint32), ref32[normal].view(np.uint32)), what
+    assert np.all(np.abs(got[~normal]) <= np.float32(2.0 ** -126)), what
+
+
+@pytest.mark.parametrize("terms", [1, 16])
+def test_every_region_short_sums(terms):
+    """dX with N = terms and dW with T = terms (each output a sum of that many
+    exact terms) over operands in every exponent region."""
+    note(f"exact grads, every region, {terms}-term sums")
+    g = np.random.default_rng(830 + terms)
+    t, n, k = 300, terms, 260
+    x = region_values((t, k), g)
+    w = region_values((n, k), g)
+    dy = small_dy((t, n), g)
+    dxo, sdx, _, _ = pam_ref.pam_exact_grads_ref(dy, x, w)
+    dx = pam.exact_grad(to_dev(dy), to_dev(w), to_dev(x)).cpu().numpy()
+    check_gemm(dx, dxo, sdx, n, "dX")
+    if terms == 1:
+        check_single_terms(dx, dxo, "dX single terms")
+    # dW: T = terms rows
+    t2, n2 = terms, 290
+    x2 = region_values((t2, k), g)
+    w2 = region_values((n2, k), g)
+    dy2 = small_dy((t2, n2), g)
+    _, _, dwo, sdw = pam_ref.pam_exact_grads_ref(dy2, x2, w2)
+    dw = pam.exact_grad(to_dev(dy2), to_dev(x2), to_dev(w2), trans_a=True).cpu().numpy()
+    check_gemm(dw, dwo, sdw, t2, "dW")
+    if terms == 1:
+        check_single_terms(dw, dwo, "dW single terms")
+
+
+def test_factor_two_to_the_128():
+    """W = 1.5 2^127 with X = 1.75 2^-10: the carry takes the factor to 2^128
+    while X .^ W = 1.25 2^118 is not clamped; dY = 2^-20 gives 2^108 exactly.
+    With X = 1.75 the product saturates and the derivative is 0."""
+    note("exact grad factor 2^128")
+    x = np.float32([[1.75 * 2.0 ** -10, 1.75, -1.75 * 2.0 ** -10]])
+    w = np.float32([[1.5 * 2.0 ** 127, 1.5 * 2.0 ** 127, -1.5 * 2.0 ** 127]])
+    dy = np.float32([[2.0 ** -20]])
+    dx = pam.exact_grad(to_dev(dy), to_dev(w), to_dev(x)).cpu().numpy()
+    assert dx.tolist() == [[2.0 ** 108, 0.0, -2.0 ** 108]]
+    dxo, _, _, _ = pam_ref.pam_exact_grads_ref(dy, x, w)
+    assert dxo.tolist() == dx.tolist()
+
+
+@pytest.mark.parametrize("share", [0.0005, 0.01, 0.2, 1.0])
+def test_extreme_mod_shares(share):
+    """X with this share of tiny / huge normals (a few per workgroup up to
+    every output: the per-output sums and the all-general workgroups), W and
+    dY ordinary, plus some tiny and huge W; split K for dW."""
+    note(f"exact grads, extreme X share {share}")
+    g = np.random.default_rng(840 + int(share * 1e4))
+    t, n, k = 700, 96, 200
+    x = g.standard_normal((t, k)).astype(np.float32)
+    pick = g.random((t, k)) < share
+    ext = region_values((t, k), g, lo_share=0.5, hi_share=0.5, zero_share=0.0)
+    x = np.where(pick, ext, x)
+    w = (g.standard_normal((n, k)) * 0.05).astype(np.float32)
+    wpick = g.random((n, k)) < 0.002
+    w = np.where(wpick, region_values((n, k), g, 0.5, 0.5, 0.0), w)
+    dy = small_dy((t, n), g)
+    dxo, sdx, dwo, sdw = pam_ref.pam_exact_grads_ref(dy, x, w)
+    xd, wd, dyd = to_dev(x), to_dev(w), to_dev(dy)
+    dx = pam.exact_grad(dyd, wd, xd).cpu().numpy()
+    dw = pam.exact_grad(dyd, xd, wd, trans_a=True).cpu().numpy()
+    check_gemm(dx, dxo, sdx, n, "dX")
+    check_gemm(dw, dwo, sdw, t, "dW")
 
 
 @pytest.mark.parametrize("t,n,k,edges", [(150, 70, 97, False), (150, 70, 97, True), (64, 128, 128, False),

@@ -43,14 +43,12 @@
  *   - Output regions overlapping an input are undefined (not checked), except
  *     that the elementwise calls (pam_mul, pam_pad, pam_palog2, pam_paexp2,
  *     pam_round_mantissa) may run in place (out == a or out == b).
- *   - Split-K plans take a temporary partial-sum buffer from the
- *     stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`),
- *     freed (stream-ordered) before the call returns, unless the caller
- *     passes a workspace (the *_ws and bf16 entry points).  On its first
- *     call on a device the library sets that device's default memory pool
- *     to keep freed memory for reuse (hipMemPoolAttrReleaseThreshold =
- *     UINT64_MAX), a process-wide setting that spares a return to the driver
- *     at every synchronisation; hipMemPoolTrimTo gives the memory back.
+ *   - The library allocates no memory.  Products that split K keep the
+ *     partial sums of the K slices in a workspace the caller passes (the
+ *     *_ws, with_plan and bf16 entry points); the entry points without a
+ *     workspace argument use the fastest plan that does not split K.
+ *   - The library keeps no state across calls but a per-thread error text
+ *     and device check; it changes no process-wide setting.
  */
 #ifndef PAM_H_
 #define PAM_H_
@@ -67,8 +65,7 @@ typedef enum {
     PAM_SUCCESS = 0,
     PAM_ERROR_INVALID_VALUE = 1, /* bad size, leading dimension, pointer or option */
     PAM_ERROR_LAUNCH = 2,        /* a HIP launch or query failed */
-    PAM_ERROR_NOT_SUPPORTED = 3, /* device is not gfx950 */
-    PAM_ERROR_ALLOC = 4          /* stream-ordered workspace allocation failed */
+    PAM_ERROR_NOT_SUPPORTED = 3  /* device is not gfx950 */
 } pam_status_t;
 
 /* An int-sized enum.  Any other value is refused with PAM_ERROR_INVALID_VALUE;
@@ -125,7 +122,8 @@ pam_status_t pam_paexp2(const float *a, float *out, int64_t n, hipStream_t strea
  * ldb >= max(1, transB == N ? n : k); ldc >= max(1, n); lda, ldb < 2^22
  * (else PAM_ERROR_NOT_SUPPORTED); A, B non-NULL when m*k resp. k*n > 0;
  * C non-NULL when m*n > 0.  m == 0 or n == 0 launches nothing; k == 0
- * writes +0.0f to C.
+ * writes +0.0f to C.  No workspace: the plan does not split K
+ * (pam_gemm_batched_ws takes one and may).
  */
 pam_status_t pam_gemm(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
                       const float *A, int64_t lda, const float *B, int64_t ldb,
@@ -136,7 +134,8 @@ pam_status_t pam_gemm(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, in
  * Sec. 3.2 (Q K^T, P V and their backward products).  Product z reads
  * A + z*strideA and B + z*strideB and writes C + z*strideC, each with the
  * layout of pam_gemm.  Strides are in elements, >= 0 (a zero A or B stride
- * broadcasts that operand); batch >= 0.  Same requirements as pam_gemm.
+ * broadcasts that operand); batch >= 0.  Same requirements as pam_gemm; no
+ * workspace, so no split K.
  */
 pam_status_t pam_gemm_batched(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
                               const float *A, int64_t lda, int64_t strideA,
@@ -162,16 +161,27 @@ typedef struct {
     int64_t whole_tiles;
 } pam_plan_t;
 
-/* The plan pam_gemm / pam_gemm_batched would use for these sizes. */
+/* The plan pam_gemm_batched_ws (and pam_gemm_workspace_size) uses for these
+ * sizes, split K allowed.  m, n, batch > 0; k >= 0. */
 pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_plan_t *plan);
+
+/* The fastest plan (by the library's cost model) whose split-K partial sums
+ * fit in max_workspace_bytes: 0 gives the plan of the entry points without a
+ * workspace argument (no split K), SIZE_MAX that of pam_gemm_plan. */
+pam_status_t pam_gemm_plan_for_workspace(int64_t m, int64_t n, int64_t k, int64_t batch,
+                                         size_t max_workspace_bytes, pam_plan_t *plan);
 
 /*
  * pam_gemm_batched with an explicit plan (for tests and tuning).
  * (tile_m, tile_n, kgroups) is (128,128,1), (128,64,1), (128,64,2),
- * (64,64,1) or (64,64,4); 1 <= splits <= 64; whole_tiles >= 0.  The result is the same
- * product as with the automatic plan, up to float32 summation order.  A plan
- * with 0 < whole_tiles < tiles runs as one launch and fails with
- * PAM_ERROR_INVALID_VALUE when its workgroups exceed 2^24 - 1.
+ * (64,64,1) or (64,64,4); 1 <= splits <= 64; whole_tiles >= 0.  The result is
+ * the same product as with the automatic plan, up to float32 summation order.
+ * A plan that splits K keeps its partial sums in `workspace`: device memory
+ * of workspace_bytes >= pam_gemm_plan_workspace_size's value, 16-byte aligned,
+ * that nothing else touches until this call's kernels on `stream` are done
+ * (NULL when that value is 0).  A plan with 0 < whole_tiles < tiles runs as
+ * one launch and fails with PAM_ERROR_INVALID_VALUE when its workgroups exceed
+ * 2^24 - 1.
  */
 pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB,
                                         int64_t m, int64_t n, int64_t k,
@@ -179,7 +189,13 @@ pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB,
                                         const float *B, int64_t ldb, int64_t strideB,
                                         float *C, int64_t ldc, int64_t strideC,
                                         int64_t batch, const pam_plan_t *plan,
+                                        void *workspace, size_t workspace_bytes,
                                         hipStream_t stream);
+
+/* Workspace bytes pam_gemm_batched_with_plan needs for these sizes under
+ * `plan` (0 when it does not split K).  m, n, k, batch >= 0 and below 2^31. */
+pam_status_t pam_gemm_plan_workspace_size(int64_t m, int64_t n, int64_t k, int64_t batch,
+                                          const pam_plan_t *plan, size_t *bytes);
 
 /*
  * Narrower-mantissa PAM matrix products (App. "PAM with Narrower
@@ -206,20 +222,23 @@ pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t m
                                 hipStream_t stream);
 
 /*
- * Exact-derivative PAM products (Table 1): the derivative of A .^ B with
- * respect to A is sgn(B) 2^(E_B + 1{M_A + M_B >= 1}), a power of two, zero
- * when A or B is zero or denormal.  This call computes
- *   C(r, c) = sum_q op(A)(r, q) * d(B(q, c) .^ Mod(r, c)) / dB(q, c)
- * for 0 <= r < m, 0 <= c < n, q < k, with float32 accumulation of exact terms
- * (a denormal op(A) element counts as zero).  For Y = X .^ W^T (X: T x K,
- * W: N x K, dY: T x N):
+ * Exact-derivative PAM products (Table 1; the true derivative of the
+ * piecewise affine product, Sec. "Derivatives"): the derivative of
+ * Mod .^ B with respect to Mod is sgn(B) 2^(E_B + 1{M_Mod + M_B >= 1}), a
+ * power of two, where Mod .^ B is not clamped, and 0 where it is: a zero or
+ * denormal Mod or B, a product that underflows to a signed zero, one that
+ * saturates at +-FLT_MAX.  This call computes
+ *   C(r, c) = sum_q op(A)(r, q) * d(Mod(r, c) .^ B(q, c)) / dMod(r, c)
+ * for 0 <= r < m, 0 <= c < n, q < k: each term exact (a denormal op(A)
+ * element counts as zero), float32 accumulation.  For Y = X .^ W^T
+ * (X: T x K, W: N x K, dY: T x N):
  *   dX = (transA = N, A = dY, B = W, Mod = X)   m = T, n = K, k = N
  *   dW = (transA = T, A = dY, B = X, Mod = W)   m = N, n = K, k = T
  * op(A) as in pam_gemm; B(q, c) = B[q*ldb + c]; Mod(r, c) = Mod[r*ldm + c];
  * C(r, c) = C[r*ldc + c] overwritten.  Requirements as pam_gemm (transB = N)
- * plus ldm >= max(1, n) and Mod non-NULL when m*n > 0.  Inf / NaN operands
- * give unspecified values.  Long K may use a stream-ordered split-K
- * workspace as pam_gemm does.
+ * plus ldm >= max(1, n) and Mod non-NULL when m*n > 0.  Every finite
+ * operand value is covered; inf / NaN operands give unspecified values.
+ * Long K may split K; without a workspace (this entry point) it does not.
  */
 pam_status_t pam_gemm_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t k,
                                  const float *A, int64_t lda, const float *B, int64_t ldb,
@@ -227,29 +246,28 @@ pam_status_t pam_gemm_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t 
                                  hipStream_t stream);
 
 /*
- * Caller-provided split-K workspace.  The matrix products above split K for
- * long-K / few-tile shapes and then take the partial sums' buffer from the
- * stream-ordered allocator (hipMallocAsync / hipFreeAsync on `stream`).  For
- * callers with their own device allocator (e.g. torch's caching allocator),
- * these entry points take the buffer instead and allocate nothing.
+ * Caller-provided split-K workspace.  For long-K / few-tile shapes the
+ * fastest plan splits K into slices whose partial sums are then added in a
+ * fixed order; these entry points take the buffer for those partial sums from
+ * the caller (e.g. from torch's caching allocator) and allocate nothing.
  *
- * pam_gemm_workspace_size: *bytes = the workspace bytes that pam_gemm,
- * pam_gemm_batched and pam_gemm_narrow (and pam_gemm_batched_ws) need for
+ * pam_gemm_workspace_size: *bytes = the workspace bytes that
+ * pam_gemm_batched_ws (and pam_gemm_batched_bf16 with a workspace) needs for
  * these sizes with the library's plan; 0 when the plan does not split K.
  * m, n, k, batch >= 0 and below 2^31; bytes non-NULL.
  *
  * pam_gemm_batched_ws: pam_gemm_narrow's product (mantissa_bits = 23:
- * pam_gemm_batched's), arguments as there, with the partial sums in
- * `workspace`: device memory of workspace_bytes bytes, 16-byte aligned, that
- * nothing else reads or writes until this call's kernels on `stream` have
- * finished (stream order: a later call on the same stream may reuse it).
- * workspace_bytes >= pam_gemm_workspace_size's value, else
- * PAM_ERROR_INVALID_VALUE before any launch; workspace may be NULL when that
- * value is 0.  The caller owns the workspace; its contents afterwards are
- * unspecified.
+ * pam_gemm_batched's), arguments as there, with the library's plan (split K
+ * allowed) and the partial sums in `workspace`: device memory of
+ * workspace_bytes bytes, 16-byte aligned, that nothing else reads or writes
+ * until this call's kernels on `stream` have finished (stream order: a later
+ * call on the same stream may reuse it).  workspace_bytes >=
+ * pam_gemm_workspace_size's value, else PAM_ERROR_INVALID_VALUE before any
+ * launch; workspace may be NULL when that value is 0.  The caller owns the
+ * workspace; its contents afterwards are unspecified.
  *
  * pam_gemm_exact_grad_workspace_size / pam_gemm_exact_grad_ws: the same for
- * pam_gemm_exact_grad.
+ * pam_gemm_exact_grad (whose plan then may split K).
  */
 pam_status_t pam_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t batch, size_t *bytes);
 
@@ -267,9 +285,8 @@ pam_status_t pam_gemm_batched_ws(pam_op_t transA, pam_op_t transB, int64_t m, in
  * in elements.  Each element is widened exactly to float32 as it is loaded;
  * the product is then pam_gemm_batched's on the widened operands, bit for bit
  * (same plan), with float32 C.  Requirements as pam_gemm_batched.  workspace
- * NULL: split-K partial sums from the stream-ordered allocator, as
- * pam_gemm_batched; otherwise as pam_gemm_batched_ws (workspace_bytes >=
- * pam_gemm_workspace_size's value).
+ * NULL: the plan of pam_gemm_batched (no split K); otherwise that of
+ * pam_gemm_batched_ws (workspace_bytes >= pam_gemm_workspace_size's value).
  */
 pam_status_t pam_gemm_batched_bf16(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
                                    const uint16_t *A, int64_t lda, int64_t strideA,
@@ -285,11 +302,13 @@ pam_status_t pam_gemm_exact_grad_ws(pam_op_t transA, int64_t m, int64_t n, int64
                                     void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
- * Figures of `device` that set the vector-ALU roofline: compute units,
- * SIMDs per compute unit and peak engine clock (kHz) read from the HIP
- * runtime and HSA, wavefront size, and the lanes a SIMD retires per clock
- * for the full-rate ops of the PAM matrix product (int32 add, float32 add,
- * mul and fma: 32 on gfx950; other vector ops retire 16).
+ * Figures of `device` that set the vector-ALU roofline: compute units and
+ * peak engine clock (kHz) from the HIP runtime, SIMDs per compute unit from
+ * HSA, the wavefront size, and the lanes a SIMD retires per clock for the
+ * full-rate ops of the PAM matrix product (int32 add, float32 add, mul and
+ * fma).  lanes_per_simd is not a device query: it is the library's constant
+ * 32 for gfx950, calibrated by issue-rate measurements (two waves per SIMD
+ * pair these ops; other vector ops retire 16).
  * valu_lane_ops_per_s = cus * simds_per_cu * lanes_per_simd * clock.
  */
 typedef struct {

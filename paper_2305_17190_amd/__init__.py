@@ -57,8 +57,8 @@ _lib = None
 
 # Every symbol include/pam.h declares.
 EXPORTS = ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm", "pam_gemm_batched",
-           "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_plan", "pam_gemm_batched_with_plan",
-           "pam_gemm_workspace_size", "pam_gemm_batched_ws", "pam_gemm_batched_bf16", "pam_gemm_exact_grad_workspace_size",
+           "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_plan", "pam_gemm_plan_for_workspace",
+           "pam_gemm_batched_with_plan", "pam_gemm_plan_workspace_size", "pam_gemm_workspace_size", "pam_gemm_batched_ws", "pam_gemm_batched_bf16", "pam_gemm_exact_grad_workspace_size",
            "pam_gemm_exact_grad_ws", "pam_device_info", "pam_status_string", "pam_last_error")
 
 
@@ -84,11 +84,13 @@ def load() -> ctypes.CDLL:
     lib.pam_gemm_exact_grad.argtypes = [i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, i64, vp]
     lib.pam_gemm.argtypes = [i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp]
     lib.pam_gemm_batched.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, vp]
-    lib.pam_gemm_batched_with_plan.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64,
-                                               i64, ctypes.POINTER(_Plan), vp]
-    lib.pam_gemm_plan.argtypes = [i64, i64, i64, i64, ctypes.POINTER(_Plan)]
-    lib.pam_device_info.argtypes = [i32, ctypes.POINTER(_DeviceInfo)]
     sz, psz = ctypes.c_size_t, ctypes.POINTER(ctypes.c_size_t)
+    lib.pam_gemm_batched_with_plan.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64,
+                                               i64, ctypes.POINTER(_Plan), vp, sz, vp]
+    lib.pam_gemm_plan_workspace_size.argtypes = [i64, i64, i64, i64, ctypes.POINTER(_Plan), psz]
+    lib.pam_gemm_plan.argtypes = [i64, i64, i64, i64, ctypes.POINTER(_Plan)]
+    lib.pam_gemm_plan_for_workspace.argtypes = [i64, i64, i64, i64, ctypes.c_size_t, ctypes.POINTER(_Plan)]
+    lib.pam_device_info.argtypes = [i32, ctypes.POINTER(_DeviceInfo)]
     lib.pam_gemm_workspace_size.argtypes = [i64, i64, i64, i64, psz]
     lib.pam_gemm_batched_ws.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i32,
                                         vp, sz, vp]
@@ -98,7 +100,8 @@ def load() -> ctypes.CDLL:
     lib.pam_gemm_exact_grad_ws.argtypes = [i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, i64, vp, sz, vp]
     for name in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm",
                  "pam_gemm_batched", "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_batched_with_plan",
-                 "pam_gemm_plan", "pam_device_info", "pam_gemm_workspace_size", "pam_gemm_batched_ws",
+                 "pam_gemm_plan_workspace_size", "pam_gemm_plan", "pam_gemm_plan_for_workspace", "pam_device_info",
+                 "pam_gemm_workspace_size", "pam_gemm_batched_ws",
                  "pam_gemm_batched_bf16",
                  "pam_gemm_exact_grad_workspace_size", "pam_gemm_exact_grad_ws"):
         getattr(lib, name).restype = i32
@@ -330,7 +333,12 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
         if plan is not None:
             full = tuple(plan) + (1, 0)[len(plan) - 3:]
             p = _Plan(*full)
-            _check(lib.pam_gemm_batched_with_plan(*args, ctypes.byref(p), _stream_handle(A)))
+            need = ctypes.c_size_t()
+            _check(lib.pam_gemm_plan_workspace_size(m, n, k, batch, ctypes.byref(p), ctypes.byref(need)))
+            keep = torch.empty(int(need.value), dtype=torch.uint8, device=A.device) if need.value else None
+            _check(lib.pam_gemm_batched_with_plan(*args, ctypes.byref(p), keep.data_ptr() if keep is not None else None,
+                                                  int(need.value), _stream_handle(A)))
+            del keep
             return out
         ws, ws_bytes, keep = _workspace("gemm", (m, n, k, batch), A.device)
         if bf16:
@@ -342,8 +350,8 @@ def bmm(A, B, trans_a: bool = False, trans_b: bool = False, out=None, plan=None,
 
 
 def exact_grad(A, B, Mod, trans_a: bool = False, out=None):
-    """C(r, c) = sum_q op(A)(r, q) d(B(q, c) .^ Mod(r, c)) / dB(q, c) (Table 1's
-    exact derivative).  For Y = X .^ W^T: dX = exact_grad(dY, W, X) and
+    """C(r, c) = sum_q op(A)(r, q) d(Mod(r, c) .^ B(q, c)) / dMod(r, c) (Table 1's
+    exact derivative: zero where Mod .^ B is clamped).  For Y = X .^ W^T: dX = exact_grad(dY, W, X) and
     dW = exact_grad(dY, X, W, trans_a=True)."""
     torch = _torch()
     _require(A, "A", 2)
@@ -371,11 +379,17 @@ def exact_grad(A, B, Mod, trans_a: bool = False, out=None):
     return out
 
 
-def plan(m: int, n: int, k: int, batch: int = 1):
+def plan(m: int, n: int, k: int, batch: int = 1, max_workspace_bytes: int | None = None):
     """(tile_m, tile_n, splits, kgroups, whole_tiles) the library picks for
-    these sizes."""
+    these sizes: with no limit (the plan gemm / bmm use, their split-K
+    workspace taken from torch), or the fastest whose split-K partial sums
+    fit in ``max_workspace_bytes`` (0: the C entry points without a
+    workspace argument)."""
     p = _Plan()
-    _check(load().pam_gemm_plan(m, n, k, batch, ctypes.byref(p)))
+    if max_workspace_bytes is None:
+        _check(load().pam_gemm_plan(m, n, k, batch, ctypes.byref(p)))
+    else:
+        _check(load().pam_gemm_plan_for_workspace(m, n, k, batch, int(max_workspace_bytes), ctypes.byref(p)))
     return (p.tile_m, p.tile_n, p.splits, p.kgroups, p.whole_tiles)
 
 

@@ -150,18 +150,77 @@ double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t k,
     return t;
 }
 
-// The cheapest plan by plan_time: for each tile shape every split count
+// How a plan's work items are launched: whole-K tiles, then `splits` slices
+// of each split tile.  A plan with whole-K tiles beside split ones runs as
+// one launch; otherwise launches take as many whole matrices as fit.
+struct Layout {
+    int64_t tiles;        // per matrix
+    int64_t total;        // tiles of the whole batch
+    int64_t splits;       // K slices of a split tile (1: none)
+    int64_t whole_tiles;  // > 0: a hybrid plan
+    int64_t per_launch;   // matrices per launch
+    int64_t ws_tiles;     // split tiles the workspace holds at once
+    size_t ws_bytes;
+};
+
+// The layout of a plan, or false (with the reason in *why) when its
+// workgroups do not fit the launch limits.
+bool layout_quiet(const Plan &plan, int64_t m, int64_t n, int64_t batch, Layout *out, const char **why) {
+    Layout L{};
+    L.tiles = ceil_div(m, plan.tile_m) * ceil_div(n, plan.tile_n);
+    if (L.tiles > kMaxDim || batch > kMaxDim * kMaxDim / L.tiles) {
+        *why = "too many output tiles (m, n or batch too large)";
+        return false;
+    }
+    L.total = L.tiles * batch;
+    L.splits = plan.splits > 1 ? plan.splits : 1;
+    if (plan.whole_tiles >= L.total)
+        L.splits = 1;
+    L.whole_tiles = L.splits > 1 ? plan.whole_tiles : 0;
+    const bool hybrid = L.whole_tiles > 0;
+    if (L.tiles * L.splits > pamk::kMaxLaunchItems ||
+        (hybrid && L.whole_tiles + (L.total - L.whole_tiles) * L.splits > pamk::kMaxLaunchItems)) {
+        *why = "too many workgroups for one launch (output too large for the plan)";
+        return false;
+    }
+    L.per_launch = hybrid ? batch : std::max<int64_t>(1, pamk::kMaxLaunchItems / (L.tiles * L.splits));
+    L.ws_tiles = hybrid ? L.total - L.whole_tiles : (L.splits > 1 ? std::min(batch, L.per_launch) * L.tiles : 0);
+    L.ws_bytes = (size_t)L.splits * (size_t)L.ws_tiles * (size_t)plan.tile_m * (size_t)plan.tile_n * sizeof(float);
+    if (L.ws_tiles == 0)
+        L.ws_bytes = 0;
+    *out = L;
+    return true;
+}
+
+pam_status_t layout_of(const Plan &plan, int64_t m, int64_t n, int64_t batch, Layout *out) {
+    const char *why = "";
+    if (!layout_quiet(plan, m, n, batch, out, &why))
+        return fail(PAM_ERROR_INVALID_VALUE, why);
+    return PAM_SUCCESS;
+}
+
+// No limit on the split-K workspace: the caller provides it.
+constexpr size_t kAnyWorkspace = ~(size_t)0;
+
+// The cheapest plan by plan_time whose split-K partial sums fit in
+// max_ws_bytes (0: no split-K): for each tile shape every split count
 // (slices of at least four chunks), and, when the tiles leave a partial last
 // round, split counts for just that round's tiles (or those of the last
 // round and a half) while the rest take the whole K.  A plan with split-K
 // must beat the best unsplit one by kSplitMargin.
-Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch) {
+Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch, size_t max_ws_bytes) {
     double best_t[2] = {0.0, 0.0};
     Plan best[2] = {};
     bool have[2] = {false, false};
     auto consider = [&](const Shape &c, const Plan &p) {
-        const double t = plan_time(c, p, m, n, k, batch);
         const int split = p.splits > 1 ? 1 : 0;
+        if (split) {
+            Layout L;
+            const char *why;
+            if (!layout_quiet(p, m, n, batch, &L, &why) || L.ws_bytes > max_ws_bytes)
+                return;
+        }
+        const double t = plan_time(c, p, m, n, k, batch);
         if (!have[split] || t < best_t[split]) {
             best_t[split] = t;
             best[split] = p;
@@ -169,7 +228,7 @@ Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch) {
         }
     };
     for (const auto &c : kShapes) {
-        const int64_t most = std::max<int64_t>(1, std::min(kMaxSplits, k / (4 * pamk::kChunkK * c.kw)));
+        const int64_t most = max_ws_bytes == 0 ? 1 : std::max<int64_t>(1, std::min(kMaxSplits, k / (4 * pamk::kChunkK * c.kw)));
         const int64_t slots = (int64_t)c.per_cu * kComputeUnits;
         const int64_t tiles = ceil_div(m, c.bm) * ceil_div(n, c.bn) * batch;
         const int64_t rest = tiles % slots;
@@ -254,67 +313,24 @@ pam_status_t check_device() {
         return fail_hip(e, "hipGetDeviceProperties");
     if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
         return fail(PAM_ERROR_NOT_SUPPORTED, std::string("device is ") + prop.gcnArchName + ", library built for gfx950");
-    // Keep freed split-K workspaces in the stream-ordered pool instead of
-    // returning them to the driver at every synchronisation.
-    hipMemPool_t pool = nullptr;
-    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess && pool != nullptr) {
-        uint64_t threshold = UINT64_MAX;
-        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &threshold);
-    }
     checked_device = dev;
     return PAM_SUCCESS;
 }
 
-// How a plan's work items are launched: whole-K tiles, then `splits` slices
-// of each split tile.  A plan with whole-K tiles beside split ones runs as
-// one launch; otherwise launches take as many whole matrices as fit.
-struct Layout {
-    int64_t tiles;        // per matrix
-    int64_t total;        // tiles of the whole batch
-    int64_t splits;       // K slices of a split tile (1: none)
-    int64_t whole_tiles;  // > 0: a hybrid plan
-    int64_t per_launch;   // matrices per launch
-    int64_t ws_tiles;     // split tiles the workspace holds at once
-    size_t ws_bytes;
-};
-
-pam_status_t layout_of(const Plan &plan, int64_t m, int64_t n, int64_t batch, Layout *out) {
-    Layout L{};
-    L.tiles = ceil_div(m, plan.tile_m) * ceil_div(n, plan.tile_n);
-    if (L.tiles > kMaxDim || batch > kMaxDim * kMaxDim / L.tiles)
-        return fail(PAM_ERROR_INVALID_VALUE, "too many output tiles (m, n or batch too large)");
-    L.total = L.tiles * batch;
-    L.splits = plan.splits > 1 ? plan.splits : 1;
-    if (plan.whole_tiles >= L.total)
-        L.splits = 1;
-    L.whole_tiles = L.splits > 1 ? plan.whole_tiles : 0;
-    const bool hybrid = L.whole_tiles > 0;
-    if (L.tiles * L.splits > pamk::kMaxLaunchItems ||
-        (hybrid && L.whole_tiles + (L.total - L.whole_tiles) * L.splits > pamk::kMaxLaunchItems))
-        return fail(PAM_ERROR_INVALID_VALUE, "too many workgroups for one launch (output too large for the plan)");
-    L.per_launch = hybrid ? batch : std::max<int64_t>(1, pamk::kMaxLaunchItems / (L.tiles * L.splits));
-    L.ws_tiles = hybrid ? L.total - L.whole_tiles : (L.splits > 1 ? std::min(batch, L.per_launch) * L.tiles : 0);
-    L.ws_bytes = (size_t)L.splits * (size_t)L.ws_tiles * (size_t)plan.tile_m * (size_t)plan.tile_n * sizeof(float);
-    if (L.ws_tiles == 0)
-        L.ws_bytes = 0;
-    *out = L;
-    return PAM_SUCCESS;
-}
-
-// A caller-provided workspace (pointer and size), or none: the library then
-// takes the split-K partial sums from the stream-ordered allocator.
+// A caller-provided workspace (pointer and size), or none (then the plan
+// does not split K).
 struct Workspace {
     void *ptr;
     size_t bytes;
 };
 
 pam_status_t check_workspace(const Workspace *ws, size_t need) {
-    if (ws == nullptr || need == 0)
+    if (need == 0)
         return PAM_SUCCESS;
     char buf[160];
-    if (ws->bytes < need) {
-        snprintf(buf, sizeof buf, "workspace of %zu bytes is smaller than the %zu this product needs", ws->bytes,
-                 need);
+    if (ws == nullptr || ws->bytes < need) {
+        snprintf(buf, sizeof buf, "workspace of %zu bytes is smaller than the %zu this product's plan needs",
+                 ws == nullptr ? (size_t)0 : ws->bytes, need);
         return fail(PAM_ERROR_INVALID_VALUE, buf);
     }
     if (ws->ptr == nullptr)
@@ -324,6 +340,8 @@ pam_status_t check_workspace(const Workspace *ws, size_t need) {
     return PAM_SUCCESS;
 }
 
+// The product under `plan`; a split plan keeps its partial sums in `ext`,
+// which must hold the plan's workspace bytes.  Allocates nothing.
 pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                       int64_t sa, const float *B, int64_t ldb, int64_t sb, float *C, int64_t ldc, int64_t sc,
                       int64_t batch, const Plan &plan, hipStream_t stream, int round_drop = 0,
@@ -368,20 +386,9 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     p.round_drop = round_drop;
     p.tiles = (int32_t)L.tiles;
     p.splits = (int32_t)L.splits;
+    float *ws = L.ws_bytes > 0 ? static_cast<float *>(ext->ptr) : nullptr;
 
-    float *ws = nullptr;
-    const bool own = L.ws_bytes > 0 && ext == nullptr;
-    if (L.ws_bytes > 0 && !own)
-        ws = static_cast<float *>(ext->ptr);
-    if (own) {
-        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), L.ws_bytes, stream);
-        if (e != hipSuccess || ws == nullptr) {
-            g_last_error = std::string("hipMallocAsync of the split-K workspace: ") + hipGetErrorString(e);
-            return PAM_ERROR_ALLOC;
-        }
-    }
-    pam_status_t result = PAM_SUCCESS;
-    for (int64_t b0 = 0; b0 < batch && result == PAM_SUCCESS; b0 += L.per_launch) {
+    for (int64_t b0 = 0; b0 < batch; b0 += L.per_launch) {
         const int64_t nb = std::min(L.per_launch, batch - b0);
         const size_t es = bf16 ? 2 : 4;   // operand element bytes
         p.A = reinterpret_cast<const float *>(reinterpret_cast<const char *>(A) + (size_t)(b0 * sa) * es);
@@ -400,22 +407,15 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
         }
         hipError_t e = pamk::launch_pam_gemm(plan.tile_m, plan.tile_n, plan.kgroups, ta == PAM_OP_T, tb == PAM_OP_T,
                                              bf16, p, stream);
-        if (e != hipSuccess) {
-            result = fail_hip(e, "gemm kernel launch");
-            break;
-        }
+        if (e != hipSuccess)
+            return fail_hip(e, "gemm kernel launch");
         if (p.split_tiles > 0) {
             e = pamk::launch_split_tile_reduce(plan.tile_m, plan.tile_n, p, stream);
             if (e != hipSuccess)
-                result = fail_hip(e, "split-K reduce launch");
+                return fail_hip(e, "split-K reduce launch");
         }
     }
-    if (own) {
-        hipError_t e = hipFreeAsync(ws, stream);
-        if (e != hipSuccess && result == PAM_SUCCESS)
-            result = fail_hip(e, "hipFreeAsync of the split-K workspace");
-    }
-    return result;
+    return PAM_SUCCESS;
 }
 
 int query_simds_per_cu(int device) {
@@ -467,6 +467,8 @@ size_t exact_grad_workspace(int64_t m, int64_t n, int64_t k, int64_t *splits_out
     return used > 1 ? (size_t)used * (size_t)m * (size_t)n * sizeof(float) : 0;
 }
 
+// ext == nullptr: one K slice (no workspace); otherwise the split plan, its
+// partial sums in *ext.
 pam_status_t run_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t k, const float *A, int64_t lda,
                             const float *B, int64_t ldb, const float *Mod, int64_t ldm, float *C, int64_t ldc,
                             hipStream_t stream, const Workspace *ext) {
@@ -479,8 +481,10 @@ pam_status_t run_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t k, co
         return PAM_SUCCESS;
     if (Mod == nullptr)
         return fail(PAM_ERROR_INVALID_VALUE, "Mod is NULL");
-    int64_t splits = 1, per = k;
-    const size_t need = k > 0 ? exact_grad_workspace(m, n, k, &splits, &per) : 0;
+    int64_t splits = 1, per = std::max<int64_t>(k, 1);
+    size_t need = 0;
+    if (k > 0 && ext != nullptr)
+        need = exact_grad_workspace(m, n, k, &splits, &per);
     st = check_workspace(ext, need);
     if (st != PAM_SUCCESS)
         return st;
@@ -502,39 +506,23 @@ pam_status_t run_exact_grad(pam_op_t transA, int64_t m, int64_t n, int64_t k, co
     p.m = (int32_t)m;
     p.n = (int32_t)n;
     p.k = (int32_t)k;
-    p.k_per_split = (int32_t)per;
+    p.k_per_split = (int32_t)std::min<int64_t>(per, kMaxDim);
     p.splits = (int32_t)splits;
     p.tiles_n = (int32_t)ceil_div(n, 128);
     p.vec_a = aligned16(A) && lda % 4 == 0;
     p.vec_b = aligned16(B) && ldb % 4 == 0;
-    float *ws = nullptr;
-    const bool own = need > 0 && ext == nullptr;
-    if (need > 0 && !own)
-        ws = static_cast<float *>(ext->ptr);
-    if (own) {
-        hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&ws), need, stream);
-        if (e != hipSuccess || ws == nullptr) {
-            g_last_error = std::string("hipMallocAsync of the split-K workspace: ") + hipGetErrorString(e);
-            return PAM_ERROR_ALLOC;
-        }
-    }
+    float *ws = need > 0 ? static_cast<float *>(ext->ptr) : nullptr;
     p.C = C;
     p.W = ws;
-    pam_status_t result = PAM_SUCCESS;
     hipError_t e = pamk::launch_pam_exact_grad(transA == PAM_OP_T, p, stream);
     if (e != hipSuccess)
-        result = fail_hip(e, "exact-derivative kernel launch");
-    else if (ws) {
+        return fail_hip(e, "exact-derivative kernel launch");
+    if (ws) {
         e = pamk::launch_splitk_reduce(ws, C, (int32_t)m, (int32_t)n, ldc, 0, p.splits, 1, stream);
         if (e != hipSuccess)
-            result = fail_hip(e, "split-K reduce launch");
+            return fail_hip(e, "split-K reduce launch");
     }
-    if (own) {
-        e = hipFreeAsync(ws, stream);
-        if (e != hipSuccess && result == PAM_SUCCESS)
-            result = fail_hip(e, "hipFreeAsync of the split-K workspace");
-    }
-    return result;
+    return PAM_SUCCESS;
 }
 
 }  // namespace
@@ -612,7 +600,7 @@ pam_status_t pam_gemm(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, in
         return st;
     if (m == 0 || n == 0)
         return PAM_SUCCESS;
-    return run_gemm(transA, transB, m, n, k, A, lda, 0, B, ldb, 0, C, ldc, 0, 1, choose_plan(m, n, k, 1), stream);
+    return run_gemm(transA, transB, m, n, k, A, lda, 0, B, ldb, 0, C, ldc, 0, 1, choose_plan(m, n, k, 1, 0), stream);
 }
 
 pam_status_t pam_gemm_batched(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k, const float *A,
@@ -624,7 +612,7 @@ pam_status_t pam_gemm_batched(pam_op_t transA, pam_op_t transB, int64_t m, int64
     if (m == 0 || n == 0 || batch == 0)
         return PAM_SUCCESS;
     return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch,
-                    choose_plan(m, n, k, batch), stream);
+                    choose_plan(m, n, k, batch, 0), stream);
 }
 
 pam_status_t pam_gemm_narrow(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k, const float *A,
@@ -639,7 +627,7 @@ pam_status_t pam_gemm_narrow(pam_op_t transA, pam_op_t transB, int64_t m, int64_
     if (m == 0 || n == 0 || batch == 0)
         return PAM_SUCCESS;
     return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch,
-                    choose_plan(m, n, k, batch), stream, 23 - mantissa_bits);
+                    choose_plan(m, n, k, batch, 0), stream, 23 - mantissa_bits);
 }
 
 pam_status_t pam_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t batch, size_t *bytes) {
@@ -655,7 +643,7 @@ pam_status_t pam_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t ba
     if (m == 0 || n == 0 || k == 0 || batch == 0)
         return PAM_SUCCESS;
     Layout L;
-    const pam_status_t st = layout_of(choose_plan(m, n, k, batch), m, n, batch, &L);
+    const pam_status_t st = layout_of(choose_plan(m, n, k, batch, kAnyWorkspace), m, n, batch, &L);
     if (st != PAM_SUCCESS)
         return st;
     *bytes = L.ws_bytes;
@@ -676,7 +664,7 @@ pam_status_t pam_gemm_batched_ws(pam_op_t transA, pam_op_t transB, int64_t m, in
         return PAM_SUCCESS;
     const Workspace ws{workspace, workspace_bytes};
     return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch,
-                    choose_plan(m, n, k, batch), stream, 23 - mantissa_bits, &ws);
+                    choose_plan(m, n, k, batch, kAnyWorkspace), stream, 23 - mantissa_bits, &ws);
 }
 
 pam_status_t pam_gemm_batched_bf16(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
@@ -692,7 +680,8 @@ pam_status_t pam_gemm_batched_bf16(pam_op_t transA, pam_op_t transB, int64_t m, 
         return PAM_SUCCESS;
     const Workspace ws{workspace, workspace_bytes};
     return run_gemm(transA, transB, m, n, k, a, lda, strideA, b, ldb, strideB, C, ldc, strideC, batch,
-                    choose_plan(m, n, k, batch), stream, 0, workspace != nullptr ? &ws : nullptr, true);
+                    choose_plan(m, n, k, batch, workspace != nullptr ? kAnyWorkspace : 0), stream, 0,
+                    workspace != nullptr ? &ws : nullptr, true);
 }
 
 pam_status_t pam_round_mantissa(const float *a, float *out, int64_t n, int32_t mantissa_bits, hipStream_t stream) {
@@ -746,7 +735,8 @@ pam_status_t pam_gemm_exact_grad_ws(pam_op_t transA, int64_t m, int64_t n, int64
     return run_exact_grad(transA, m, n, k, A, lda, B, ldb, Mod, ldm, C, ldc, stream, &ws);
 }
 
-pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_plan_t *plan) {
+pam_status_t pam_gemm_plan_for_workspace(int64_t m, int64_t n, int64_t k, int64_t batch, size_t max_workspace_bytes,
+                                         pam_plan_t *plan) {
     if (plan == nullptr)
         return fail(PAM_ERROR_INVALID_VALUE, "plan is NULL");
     if (m <= 0 || n <= 0 || k < 0 || batch <= 0)
@@ -755,7 +745,7 @@ pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_p
         return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
     if (check_output_size(m, n, batch) != PAM_SUCCESS)
         return PAM_ERROR_INVALID_VALUE;
-    const Plan p = choose_plan(m, n, std::max<int64_t>(k, 1), batch);
+    const Plan p = choose_plan(m, n, std::max<int64_t>(k, 1), batch, max_workspace_bytes);
     plan->tile_m = p.tile_m;
     plan->tile_n = p.tile_n;
     plan->splits = p.splits;
@@ -764,13 +754,12 @@ pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_p
     return PAM_SUCCESS;
 }
 
-pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
-                                        const float *A, int64_t lda, int64_t strideA, const float *B, int64_t ldb,
-                                        int64_t strideB, float *C, int64_t ldc, int64_t strideC, int64_t batch,
-                                        const pam_plan_t *plan, hipStream_t stream) {
-    pam_status_t st = validate(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch);
-    if (st != PAM_SUCCESS)
-        return st;
+pam_status_t pam_gemm_plan(int64_t m, int64_t n, int64_t k, int64_t batch, pam_plan_t *plan) {
+    return pam_gemm_plan_for_workspace(m, n, k, batch, kAnyWorkspace, plan);
+}
+
+// The plan of `plan` for these sizes (tile shape and split count checked).
+pam_status_t plan_from(const pam_plan_t *plan, int64_t k, Plan *out) {
     if (plan == nullptr)
         return fail(PAM_ERROR_INVALID_VALUE, "plan is NULL");
     const bool tile_ok = (plan->kgroups == 1 && ((plan->tile_m == 128 && plan->tile_n == 128) ||
@@ -786,8 +775,6 @@ pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB, int64_
         return fail(PAM_ERROR_INVALID_VALUE, "splits must be in [1, 64]");
     if (plan->whole_tiles < 0)
         return fail(PAM_ERROR_INVALID_VALUE, "whole_tiles must be >= 0");
-    if (m == 0 || n == 0 || batch == 0)
-        return PAM_SUCCESS;
     Plan p{plan->tile_m, plan->tile_n, plan->kgroups, 1, std::max<int64_t>(k, 1), 0};
     if (plan->splits > 1 && k > 0) {
         const int64_t per = ceil_div(ceil_div(k, plan->splits), pamk::kChunkK) * pamk::kChunkK;
@@ -795,7 +782,52 @@ pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB, int64_
         p.splits = (int)ceil_div(k, per);
         p.whole_tiles = plan->whole_tiles;
     }
-    return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch, p, stream);
+    *out = p;
+    return PAM_SUCCESS;
+}
+
+pam_status_t pam_gemm_plan_workspace_size(int64_t m, int64_t n, int64_t k, int64_t batch, const pam_plan_t *plan,
+                                          size_t *bytes) {
+    if (bytes == nullptr)
+        return fail(PAM_ERROR_INVALID_VALUE, "bytes is NULL");
+    *bytes = 0;
+    if (m < 0 || n < 0 || k < 0 || batch < 0)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n, k and batch must be >= 0");
+    if (m > kMaxDim || n > kMaxDim || k > kMaxDim)
+        return fail(PAM_ERROR_INVALID_VALUE, "m, n and k must be below 2^31");
+    if (check_output_size(m, n, batch) != PAM_SUCCESS)
+        return PAM_ERROR_INVALID_VALUE;
+    Plan p;
+    pam_status_t st = plan_from(plan, k, &p);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (m == 0 || n == 0 || k == 0 || batch == 0)
+        return PAM_SUCCESS;
+    Layout L;
+    st = layout_of(p, m, n, batch, &L);
+    if (st != PAM_SUCCESS)
+        return st;
+    *bytes = L.ws_bytes;
+    return PAM_SUCCESS;
+}
+
+pam_status_t pam_gemm_batched_with_plan(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                                        const float *A, int64_t lda, int64_t strideA, const float *B, int64_t ldb,
+                                        int64_t strideB, float *C, int64_t ldc, int64_t strideC, int64_t batch,
+                                        const pam_plan_t *plan, void *workspace, size_t workspace_bytes,
+                                        hipStream_t stream) {
+    pam_status_t st = validate(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch);
+    if (st != PAM_SUCCESS)
+        return st;
+    Plan p;
+    st = plan_from(plan, k, &p);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (m == 0 || n == 0 || batch == 0)
+        return PAM_SUCCESS;
+    const Workspace ws{workspace, workspace_bytes};
+    return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch, p, stream, 0,
+                    &ws);
 }
 
 pam_status_t pam_device_info(int device, pam_device_info_t *info) {
@@ -834,8 +866,6 @@ const char *pam_status_string(pam_status_t s) {
         return "PAM_ERROR_LAUNCH";
     case PAM_ERROR_NOT_SUPPORTED:
         return "PAM_ERROR_NOT_SUPPORTED";
-    case PAM_ERROR_ALLOC:
-        return "PAM_ERROR_ALLOC";
     }
     return "PAM_ERROR_UNKNOWN";
 }

@@ -9,7 +9,9 @@
  * Cases: pam_mul (bit-exact, including zeros, denormals, inf, NaN and a tail
  * of 3 elements); pam_gemm with op(B) transposed on a ragged shape;
  * pam_gemm_batched_ws with a caller workspace on a long-K batched shape whose
- * plan splits K; pam_gemm_batched on the same shape; one refused argument.
+ * plan splits K; pam_gemm_batched on the same shape (no workspace: its plan
+ * keeps K whole), against the oracle and against that plan forced through
+ * pam_gemm_batched_with_plan bit for bit; one refused argument.
  * GEMM tolerance: |C - C_ref| <= 1e-5 sqrt(K) S + K 2^-126 per element, with
  * S = sum of |terms| (the oracle's float64 sums).
  */
@@ -219,16 +221,32 @@ static void check_gemm_batched_ws(hipStream_t stream) {
     CHECK_HIP(hipStreamSynchronize(stream));
     CHECK_HIP(hipMemcpy(c, dc, batch * sc * sizeof(float), hipMemcpyDeviceToHost));
     compare_gemm("pam_gemm_batched_ws 3x70x90x12000", c, 0, 0, m, n, k, a, k, sa, b, n, sb, batch, n, sc);
-    /* the allocating entry point: the same plan, so the same bits */
-    float *c2 = malloc(batch * sc * sizeof(float));
+    /* the entry point without a workspace: the plan that keeps K whole, the
+       same bits as that plan forced through pam_gemm_batched_with_plan */
+    float *c2 = malloc(batch * sc * sizeof(float)), *c3 = malloc(batch * sc * sizeof(float));
     CHECK_HIP(hipMemset(dc, 0xFF, batch * sc * sizeof(float)));
     CHECK_PAM(pam_gemm_batched(PAM_OP_N, PAM_OP_N, m, n, k, da, k, sa, db, n, sb, dc, n, sc, batch, stream));
     CHECK_HIP(hipStreamSynchronize(stream));
     CHECK_HIP(hipMemcpy(c2, dc, batch * sc * sizeof(float), hipMemcpyDeviceToHost));
-    if (memcmp(c, c2, batch * sc * sizeof(float)) != 0) {
-        fprintf(stderr, "pam_gemm_batched and pam_gemm_batched_ws differ\n");
+    compare_gemm("pam_gemm_batched 3x70x90x12000", c2, 0, 0, m, n, k, a, k, sa, b, n, sb, batch, n, sc);
+    pam_plan_t whole;
+    CHECK_PAM(pam_gemm_plan_for_workspace(m, n, k, batch, 0, &whole));
+    size_t whole_bytes = 1;
+    CHECK_PAM(pam_gemm_plan_workspace_size(m, n, k, batch, &whole, &whole_bytes));
+    if (whole.splits != 1 || whole_bytes != 0) {
+        fprintf(stderr, "the plan without a workspace splits K\n");
         failures++;
     }
+    CHECK_HIP(hipMemset(dc, 0xFF, batch * sc * sizeof(float)));
+    CHECK_PAM(pam_gemm_batched_with_plan(PAM_OP_N, PAM_OP_N, m, n, k, da, k, sa, db, n, sb, dc, n, sc, batch, &whole,
+                                         NULL, 0, stream));
+    CHECK_HIP(hipStreamSynchronize(stream));
+    CHECK_HIP(hipMemcpy(c3, dc, batch * sc * sizeof(float), hipMemcpyDeviceToHost));
+    if (memcmp(c2, c3, batch * sc * sizeof(float)) != 0) {
+        fprintf(stderr, "pam_gemm_batched and its plan forced differ\n");
+        failures++;
+    }
+    free(c3);
     CHECK_HIP(hipFree(ws));
     CHECK_HIP(hipFree(da));
     CHECK_HIP(hipFree(db));

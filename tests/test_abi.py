@@ -41,7 +41,8 @@ def test_every_declared_symbol_is_exported(lib):
 def test_status_strings(lib):
     assert lib.pam_status_string(0) == b"PAM_SUCCESS"
     assert lib.pam_status_string(1) == b"PAM_ERROR_INVALID_VALUE"
-    assert lib.pam_status_string(4) == b"PAM_ERROR_ALLOC"
+    assert lib.pam_status_string(3) == b"PAM_ERROR_NOT_SUPPORTED"
+    assert lib.pam_status_string(4) == b"PAM_ERROR_UNKNOWN"     # the library allocates nothing: no such status
 
 
 def gemm_call(lib, **kw):
@@ -129,7 +130,34 @@ def test_plan_selection_is_host_logic(lib):
                                   (64, 64, 65, 1), (128, 128, 2, 1, -1)])
 def test_with_plan_rejects_bad_tiles(lib, plan):
     P = pam._Plan(*plan)
-    assert lib.pam_gemm_batched_with_plan(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1, ctypes.byref(P), None) == 1
+    assert lib.pam_gemm_batched_with_plan(0, 0, 4, 4, 4, 8, 4, 16, 8, 4, 16, 8, 4, 16, 1, ctypes.byref(P),
+                                          None, 0, None) == 1
+    out = ctypes.c_size_t()
+    assert lib.pam_gemm_plan_workspace_size(4, 4, 4, 1, ctypes.byref(P), ctypes.byref(out)) == 1
+
+
+def test_with_plan_split_needs_its_workspace(lib):
+    """A forced split plan takes its partial sums from the caller: its size is
+    splits x split tiles x tile, and a smaller or missing workspace is refused
+    before any launch (fake, never dereferenced pointers)."""
+    m, n, k = 300, 200, 4000
+    out = ctypes.c_size_t()
+    P = pam._Plan(128, 64, 4, 1, 0)
+    assert lib.pam_gemm_plan_workspace_size(m, n, k, 1, ctypes.byref(P), ctypes.byref(out)) == 0
+    assert out.value == 4 * 3 * 4 * 128 * 64 * 4
+    args = (0, 0, m, n, k, 256, k, 0, 256, n, 0, 256, n, 0, 1, ctypes.byref(P))
+    assert lib.pam_gemm_batched_with_plan(*args, None, 0, None) == 1
+    assert b"smaller" in lib.pam_last_error()
+    assert lib.pam_gemm_batched_with_plan(*args, 4096, out.value - 1, None) == 1
+    assert lib.pam_gemm_batched_with_plan(*args, 4100, out.value, None) == 1
+    assert b"aligned" in lib.pam_last_error()
+    P1 = pam._Plan(128, 64, 1, 1, 0)
+    assert lib.pam_gemm_plan_workspace_size(m, n, k, 1, ctypes.byref(P1), ctypes.byref(out)) == 0
+    assert out.value == 0
+    # hybrid: the first 10 of 12 tiles whole, the last 2 in 4 slices
+    P2 = pam._Plan(128, 64, 4, 1, 10)
+    assert lib.pam_gemm_plan_workspace_size(m, n, k, 1, ctypes.byref(P2), ctypes.byref(out)) == 0
+    assert out.value == 4 * 2 * 128 * 64 * 4
 
 
 def test_leading_dimension_limit(lib):

@@ -90,8 +90,11 @@ def test_bf16_c_abi_workspace_modes():
                                          c.data_ptr(), n, m * n, batch, w, nbytes, stream) == 0
         outs.append(c)
     torch.cuda.synchronize()
-    assert torch.equal(outs[0].view(torch.int32), outs[1].view(torch.int32))
-    assert torch.equal(outs[0].view(torch.int32), pam.bmm(a.float(), b.float()).view(torch.int32))
+    # without a workspace: the plan that keeps K whole; with one: the library's plan
+    free_plan = pam.plan(m, n, k, batch, max_workspace_bytes=0)
+    assert free_plan[2] == 1 and pam.plan(m, n, k, batch)[2] > 1
+    assert torch.equal(outs[0].view(torch.int32), pam.bmm(a.float(), b.float(), plan=free_plan).view(torch.int32))
+    assert torch.equal(outs[1].view(torch.int32), pam.bmm(a.float(), b.float()).view(torch.int32))
 
 
 def test_bf16_argument_rules():

@@ -1,7 +1,8 @@
 """The library through its C ABI alone: tests/c_abi_check.c (plain C, no
 Python or torch in the process) allocates with hipMalloc, calls pam_mul,
-pam_gemm, pam_gemm_batched_ws and pam_gemm_batched, and compares with the C
-oracle (bit-exact elementwise, the GEMM tolerance for the products)."""
+pam_gemm, pam_gemm_batched_ws, pam_gemm_batched and
+pam_gemm_batched_with_plan, and compares with the C oracle (bit-exact
+elementwise, the GEMM tolerance for the products)."""
 import os
 import subprocess
 import sys

@@ -67,6 +67,30 @@ def inject_zeros_and_tiny(x: np.ndarray, frac_zero: float, frac_tiny: float, see
     return x
 
 
+def exact_sum_values(shape, seed: int, frac_zero: float = 0.001, frac_tiny: float = 0.001) -> np.ndarray:
+    """float32 values with two mantissa bits and exponents in [-6, -3]:
+    (-1)^s 2^e (1 + j/4).  Any sum of products of such values (PAM or true
+    products: both are multiples of 2^-14 below 2^-4) stays exact in float32
+    for up to 2^16 terms, in every summation order.  Planted: signed zeros,
+    denormals, and tiny normals (+-u 2^-126, u in [1, 4)) that vanish in every
+    such product, so the exact-sum property holds while the zero and tiny
+    values still appear in the operands.
+    """
+    g = rng(seed)
+    e = g.integers(-6, -2, size=shape)
+    j = g.integers(0, 4, size=shape)
+    sgn = np.where(g.random(shape) < 0.5, -1.0, 1.0)
+    x = (sgn * np.ldexp(1.0 + j / 4.0, e)).astype(np.float32)
+    u = g.random(shape)
+    tiny = (sgn * g.uniform(1.0, 4.0, size=shape) * MIN_NORMAL_F32).astype(np.float32)
+    denorm = (sgn * g.uniform(0.01, 0.99, size=shape) * MIN_NORMAL_F32).astype(np.float32)
+    zero = np.where(sgn < 0, np.float32(-0.0), np.float32(0.0)).astype(np.float32)
+    x = np.where(u < frac_zero, zero, x)
+    x = np.where((u >= frac_zero) & (u < frac_zero + frac_tiny / 2), denorm, x)
+    x = np.where((u >= frac_zero + frac_tiny / 2) & (u < frac_zero + frac_tiny), tiny, x)
+    return x.astype(np.float32)
+
+
 def row_softmax(logits: np.ndarray) -> np.ndarray:
     """Ordinary float32 softmax along the last axis (data generation only)."""
     m = logits.max(axis=-1, keepdims=True)

@@ -279,6 +279,29 @@ pam_status_t pam_gemm_batched_ws(pam_op_t transA, pam_op_t transB, int64_t m, in
                                  void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * For callers that cannot allocate device memory or pass a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): pam_gemm_batched_ws's product without a workspace argument.
+ * Split-K partial sums go to a static scratch of 64 MiB in device memory
+ * that the library holds on every device it runs on until the process ends
+ * (no hipMalloc, hipFree or other allocation by this call).  The plan is the
+ * fastest whose partial sums fit in the scratch (pam_gemm_plan_for_workspace
+ * with 64 MiB): pam_gemm_plan's when its workspace is at most 64 MiB, else a
+ * shorter split, else none; a plan needing more is refused with
+ * PAM_ERROR_INVALID_VALUE (never chosen).  Arguments as pam_gemm_batched_ws
+ * without workspace and workspace_bytes.  Every call on a device shares that
+ * device's scratch and leaves its contents behind (each call writes every
+ * partial sum it reads, so nothing must start at zero): calls that overlap
+ * on one device -- on different streams or from different threads -- race;
+ * serialize them (one stream, or events).
+ */
+pam_status_t pam_gemm_batched_noalloc(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                                      const float *A, int64_t lda, int64_t strideA,
+                                      const float *B, int64_t ldb, int64_t strideB,
+                                      float *C, int64_t ldc, int64_t strideC,
+                                      int64_t batch, int32_t mantissa_bits, hipStream_t stream);
+
+/*
  * bfloat16 operands (App. "PAM with Narrower Mantissas"; storage of 7-bit
  * mantissa operands in half the bytes): A and B hold bfloat16 values (the
  * high 16 bits of float32 encodings), leading dimensions and batch strides

@@ -58,8 +58,10 @@ _lib = None
 # Every symbol include/pam.h declares.
 EXPORTS = ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm", "pam_gemm_batched",
            "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_plan", "pam_gemm_plan_for_workspace",
-           "pam_gemm_batched_with_plan", "pam_gemm_plan_workspace_size", "pam_gemm_workspace_size", "pam_gemm_batched_ws", "pam_gemm_batched_bf16", "pam_gemm_exact_grad_workspace_size",
-           "pam_gemm_exact_grad_ws", "pam_device_info", "pam_status_string", "pam_last_error")
+           "pam_gemm_batched_with_plan", "pam_gemm_plan_workspace_size", "pam_gemm_workspace_size",
+           "pam_gemm_batched_ws", "pam_gemm_batched_noalloc", "pam_gemm_batched_bf16",
+           "pam_gemm_exact_grad_workspace_size", "pam_gemm_exact_grad_ws", "pam_device_info", "pam_status_string",
+           "pam_last_error")
 
 
 def library_path() -> str:
@@ -94,6 +96,8 @@ def load() -> ctypes.CDLL:
     lib.pam_gemm_workspace_size.argtypes = [i64, i64, i64, i64, psz]
     lib.pam_gemm_batched_ws.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i32,
                                         vp, sz, vp]
+    lib.pam_gemm_batched_noalloc.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64,
+                                             i32, vp]
     lib.pam_gemm_batched_bf16.argtypes = [i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64, i64, i64,
                                           vp, sz, vp]
     lib.pam_gemm_exact_grad_workspace_size.argtypes = [i64, i64, i64, psz]
@@ -101,7 +105,7 @@ def load() -> ctypes.CDLL:
     for name in ("pam_mul", "pam_pad", "pam_palog2", "pam_paexp2", "pam_round_mantissa", "pam_gemm",
                  "pam_gemm_batched", "pam_gemm_narrow", "pam_gemm_exact_grad", "pam_gemm_batched_with_plan",
                  "pam_gemm_plan_workspace_size", "pam_gemm_plan", "pam_gemm_plan_for_workspace", "pam_device_info",
-                 "pam_gemm_workspace_size", "pam_gemm_batched_ws",
+                 "pam_gemm_workspace_size", "pam_gemm_batched_ws", "pam_gemm_batched_noalloc",
                  "pam_gemm_batched_bf16",
                  "pam_gemm_exact_grad_workspace_size", "pam_gemm_exact_grad_ws"):
         getattr(lib, name).restype = i32

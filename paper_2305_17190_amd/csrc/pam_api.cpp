@@ -630,6 +630,44 @@ pam_status_t pam_gemm_narrow(pam_op_t transA, pam_op_t transB, int64_t m, int64_
                     choose_plan(m, n, k, batch, 0), stream, 23 - mantissa_bits);
 }
 
+pam_status_t pam_gemm_batched_noalloc(pam_op_t transA, pam_op_t transB, int64_t m, int64_t n, int64_t k,
+                                      const float *A, int64_t lda, int64_t strideA, const float *B, int64_t ldb,
+                                      int64_t strideB, float *C, int64_t ldc, int64_t strideC, int64_t batch,
+                                      int32_t mantissa_bits, hipStream_t stream) {
+    if (mantissa_bits < 0 || mantissa_bits > 23)
+        return fail(PAM_ERROR_INVALID_VALUE, "mantissa_bits must be in [0, 23]");
+    pam_status_t st = validate(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch);
+    if (st != PAM_SUCCESS)
+        return st;
+    if (m == 0 || n == 0 || batch == 0)
+        return PAM_SUCCESS;
+    const Plan plan = choose_plan(m, n, std::max<int64_t>(k, 1), batch, pamk::kScratchBytes);
+    Layout L{};
+    if (k > 0) {
+        st = layout_of(plan, m, n, batch, &L);
+        if (st != PAM_SUCCESS)
+            return st;
+        if (L.ws_bytes > pamk::kScratchBytes) {
+            char buf[160];
+            snprintf(buf, sizeof buf, "split-K partial sums of %zu bytes exceed the %zu-byte static scratch",
+                     L.ws_bytes, pamk::kScratchBytes);
+            return fail(PAM_ERROR_INVALID_VALUE, buf);
+        }
+    }
+    st = check_device();
+    if (st != PAM_SUCCESS)
+        return st;
+    void *scratch = nullptr;
+    if (L.ws_bytes > 0) {
+        const hipError_t e = pamk::scratch_address(&scratch);
+        if (e != hipSuccess)
+            return fail_hip(e, "hipGetSymbolAddress of the static scratch");
+    }
+    const Workspace ws{scratch, pamk::kScratchBytes};
+    return run_gemm(transA, transB, m, n, k, A, lda, strideA, B, ldb, strideB, C, ldc, strideC, batch, plan, stream,
+                    23 - mantissa_bits, &ws);
+}
+
 pam_status_t pam_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t batch, size_t *bytes) {
     if (bytes == nullptr)
         return fail(PAM_ERROR_INVALID_VALUE, "bytes is NULL");

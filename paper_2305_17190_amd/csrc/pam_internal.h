@@ -62,6 +62,11 @@ hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bo
 // over s = 0, 1, ... of W[s][t][.][.], in that order.
 hipError_t launch_split_tile_reduce(int tile_m, int tile_n, const GemmParams &p, hipStream_t stream);
 
+// Bytes of the static split-K scratch pam_gemm_batched_noalloc uses, and its
+// device address on the current device (looked up once per device).
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+hipError_t scratch_address(void **out);
+
 // Workgroups one matrix product launch may hold (its grid, in threads, stays
 // below 2^32).
 constexpr int64_t kMaxLaunchItems = 16777215;

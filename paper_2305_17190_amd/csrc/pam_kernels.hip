@@ -55,6 +55,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "pam_internal.h"
 #include "pam_tile.h"
@@ -636,6 +637,45 @@ hipError_t launch_fill_zero(float *C, int32_t m, int32_t n, int64_t ldc, int64_t
     const int64_t blocks = std::min<int64_t>((total + 255) / 256, 256 * 32);
     hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, C, m, n, ldc, strideC, total);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Static split-K scratch of pam_gemm_batched_noalloc
+// ---------------------------------------------------------------------------
+
+// File-scope device memory: every device the library runs on holds one copy
+// until the process ends.  Host code must not pass `scratch` itself to a
+// kernel or a copy (on the host it names a stand-in, not device memory): the
+// device address comes from hipGetSymbolAddress, per device.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t scratch_address(void **out) {
+    *out = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= kMaxDevices)
+        return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        // Once per device, with that device current (hipGetDevice above).
+        void *ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess)
+            return e;
+        if (ptr == nullptr)
+            return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 }  // namespace pamk

@@ -50,8 +50,10 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def committed_traffic(workload: str, form: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary.
+def committed_counter(workload: str, form: str, key: str):
+    """A per-launch figure from the committed rocprofv3 counter summary of one
+    product (``traffic_bytes_per_launch``: HBM bytes; ``sustained_clock_ghz``:
+    the engine clock the counters saw while the kernel ran).
 
     Returns None when there is no summary for this kernel or the kernel
     source changed since the counters were taken.
@@ -62,7 +64,7 @@ def committed_traffic(workload: str, form: str):
     with open(path) as f:
         text = f.read()
     sha = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
-    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    val = re.search(key + r":\s*([0-9.eE+]+)", text)
     if not sha or not val or sha.group(1) != kernel_source_digest():
         return None
     return float(val.group(1))
@@ -339,18 +341,22 @@ def main() -> int:
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
-    per_form = {}
+    per_form, med_form = {}, {}
     for f in forms:
-        ms = [s.elapsed_time(e) for s, e in events[f.name]]
+        ms = sorted(s.elapsed_time(e) for s, e in events[f.name])
         per_form[f.name] = sum(ms) / len(ms)
+        med_form[f.name] = ms[len(ms) // 2] if len(ms) % 2 else 0.5 * (ms[len(ms) // 2 - 1] + ms[len(ms) // 2])
         log(f"  {f.name:6s} m={f.m} n={f.n} k={f.k} batch={f.batch} plan={pam.plan(f.m, f.n, f.k, f.batch)} "
-            f"avg {per_form[f.name]:.3f} ms  {f.macs / per_form[f.name] / 1e9:.1f} GPAM-MAC/s")
+            f"avg {per_form[f.name]:.3f} ms median {med_form[f.name]:.3f} ms  "
+            f"{f.macs / med_form[f.name] / 1e9:.1f} GPAM-MAC/s")
 
     info = pam.device_info(0)
     peak = NOMINAL_VALU_LANE_OPS
     dom = max(forms, key=lambda f: per_form[f.name] * 1.0)
     dom_s = per_form[dom.name] / 1e3
     achieved = ALGO_LANE_OPS_PER_MAC * dom.macs / dom_s
+    achieved_median = ALGO_LANE_OPS_PER_MAC * dom.macs / (med_form[dom.name] / 1e3)
+    clock_ghz = committed_counter(spec["name"], dom.name, "sustained_clock_ghz")
     value = macs_per_step * args.steps / elapsed / 1e9
     log(f"device: {info}")
     log(f"step {elapsed / args.steps * 1e3:.3f} ms, {value:.1f} GPAM-MAC/s; dominant {dom.name}: "
@@ -386,11 +392,22 @@ def main() -> int:
             "peak": round(peak / 1e12, 3),
             "unit": "Tlane-op/s",
             "frac": round(achieved / peak, 4),
-            "traffic": committed_traffic(spec["name"], dom.name),
+            "traffic": committed_counter(spec["name"], dom.name, "traffic_bytes_per_launch"),
             "lane_ops_per_mac": ALGO_LANE_OPS_PER_MAC,
             "avg_launch_ms": round(per_form[dom.name], 4),
+            "median_launch_ms": round(med_form[dom.name], 4),
+            "frac_median": round(achieved_median / peak, 4),
             "device_peak": round(info["valu_lane_ops_per_s"] / 1e12, 3),
+            # the engine clock rocprofv3's counters saw for this kernel (the
+            # chip runs below its 2.4 GHz peak under this load), and the
+            # fraction of the peak priced at that clock
+            "sustained_clock_ghz": clock_ghz,
+            "frac_at_sustained_clock": (round(achieved / (peak * clock_ghz / 2.4), 4) if clock_ghz else None),
         },
+        "products": {f.name: {"median_ms": round(med_form[f.name], 4), "avg_ms": round(per_form[f.name], 4),
+                              "gpam_mac_s": round(f.macs / med_form[f.name] / 1e6, 1),
+                              "frac": round(ALGO_LANE_OPS_PER_MAC * f.macs / (med_form[f.name] / 1e3) / peak, 4)}
+                     for f in forms},
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")

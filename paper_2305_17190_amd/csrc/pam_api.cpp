@@ -58,30 +58,30 @@ struct Shape {
 // (more waves without partial sums in HBM: the groups add their partial
 // tiles in LDS, at more staging work per MAC).  The 128 x 128 tile holds
 // three waves per SIMD, the others two.
-const Shape kShapes[] = {{128, 128, 1, 4, 3, 26.67e12},
-                         {128, 64, 1, 2, 4, 20.49e12},
-                         {128, 64, 2, 4, 2, 20.6e12},
-                         {64, 64, 1, 1, 8, 19.64e12},
-                         {64, 64, 4, 4, 2, 15.99e12}};
+const Shape kShapes[] = {{128, 128, 1, 4, 3, 26.83e12},
+                         {128, 64, 1, 2, 4, 22.15e12},
+                         {128, 64, 2, 4, 2, 20.5e12},
+                         {64, 64, 1, 1, 8, 20.64e12},
+                         {64, 64, 4, 4, 2, 17.39e12}};
 constexpr int kComputeUnits = 256;
 constexpr int kSimdsPerCu = 4;
 // Vector-ALU throughput of one SIMD holding 0..3 waves of this kernel,
 // relative to three: one wave issues alone, two pair their adds and fmas
 // but leave barrier and LDS waits exposed.
-constexpr double kSimdEfficiency[4] = {0.0, 0.4132, 0.8558, 1.0};
-constexpr double kWorkgroupFixedS = 5.0e-6;  // first loads, epilogue stores
-constexpr double kSplitFixedS = 9.0e-6;      // second launch, workspace
+constexpr double kSimdEfficiency[4] = {0.0, 0.4161, 0.8558, 1.0};
+constexpr double kWorkgroupFixedS = 5.6e-6;  // first loads, epilogue stores
+constexpr double kSplitFixedS = 6.8e-6;      // second launch, workspace
 // Effective rate of writing and re-reading partial sums: up to a few hundred
 // MB they largely stay in the last-level cache, so above the HBM rate.
-constexpr double kPartialBytesPerS = 9.6e12;
+constexpr double kPartialBytesPerS = 10.6e12;
 // Workgroups start as soon as slots free up, so a partial last round costs
 // less than a full one the more rounds precede it (they end staggered).
-constexpr double kTailDamping = 0.4829;
+constexpr double kTailDamping = 0.4778;
 // Compute units run at different clocks under load, so the last round of
 // workgroups does not end at once: the launch ends this fraction of one
 // workgroup's duration after the average, scaled by how many slots the last
 // round leaves without a shorter partial-round workgroup to absorb it.
-constexpr double kRoundImbalance = 0.0788;
+constexpr double kRoundImbalance = 0.078;
 // Split-K plans must beat the best unsplit plan by this factor (they change
 // the summation order and take a workspace).
 constexpr double kSplitMargin = 0.97;
@@ -89,7 +89,7 @@ constexpr double kSplitMargin = 0.97;
 // offers them up to this many tiles.
 constexpr int64_t kMaxHybridTiles = 1 << 20;
 // Split counts the plan search considers.
-constexpr int kSplitChoices[] = {1, 2, 3, 4, 5, 6, 7, 8, 12, 16, 24, 32, 48, 64};
+constexpr int kSplitChoices[] = {1, 2, 3, 4, 5, 6, 7, 8, 12, 16, 24, 32, 48, 56, 64};
 
 double cu_efficiency(int waves_per_cu) {
     const int base = waves_per_cu / kSimdsPerCu;

@@ -577,8 +577,25 @@ __global__ void __launch_bounds__(256) split_tile_reduce_kernel(GemmParams p, in
             continue;
         const float *w = p.W + t * tile_elems + r * bn + c;
         float4 sum = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        for (int q = 0; q < p.splits; ++q) {
-            const float4 x = *reinterpret_cast<const float4 *>(w + q * slice);
+        // Eight slices' loads in flight before their adds (in slice order):
+        // a thread's loads are independent, only the sum is sequential.
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        int q = 0;
+        for (; q + 8 <= p.splits; q += 8) {
+            f32x4 x[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                x[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(w + (q + u) * slice));
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                sum.x += x[u].x;
+                sum.y += x[u].y;
+                sum.z += x[u].z;
+                sum.w += x[u].w;
+            }
+        }
+        for (; q < p.splits; ++q) {
+            const f32x4 x = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(w + q * slice));
             sum.x += x.x;
             sum.y += x.y;
             sum.z += x.z;

@@ -20,18 +20,19 @@ def test_more_than_one_gpu_is_refused():
     assert r.stdout == ""
 
 
-def test_committed_traffic_follows_the_kernel_digest(tmp_path, monkeypatch):
+def test_committed_counters_follow_the_kernel_digest(tmp_path, monkeypatch):
     digest = bench.kernel_source_digest()
     prof = tmp_path / "profiles"
     prof.mkdir()
     (prof / "traffic_wX_fwd.md").write_text(
-        f"traffic_bytes_per_launch: 1.5e+09\nkernel_source_sha256_16: {digest}\n")
+        f"traffic_bytes_per_launch: 1.5e+09\nsustained_clock_ghz: 2.05\nkernel_source_sha256_16: {digest}\n")
     (prof / "traffic_wX_dX.md").write_text(
         "traffic_bytes_per_launch: 1.5e+09\nkernel_source_sha256_16: 0000000000000000\n")
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    assert bench.committed_traffic("wX", "fwd") == 1.5e9
-    assert bench.committed_traffic("wX", "dX") is None      # measured on another kernel source
-    assert bench.committed_traffic("wX", "dW") is None      # never measured
+    assert bench.committed_counter("wX", "fwd", "traffic_bytes_per_launch") == 1.5e9
+    assert bench.committed_counter("wX", "fwd", "sustained_clock_ghz") == 2.05
+    assert bench.committed_counter("wX", "dX", "traffic_bytes_per_launch") is None   # another kernel source
+    assert bench.committed_counter("wX", "dW", "traffic_bytes_per_launch") is None   # never measured
 
 
 def test_cpu_baseline_fields():

@@ -86,3 +86,32 @@ def test_repeatable_and_stream_ordered():
     s.synchronize()
     assert torch.equal(o1.view(torch.int32), o2.view(torch.int32))
     assert_bits_equal(o1.cpu().numpy(), pam_ref.pam_mul_ref(a, b), "side stream")
+
+
+EVERY_A_B = {
+    "1.5": 0x3FC00000, "-1": 0xBF800000, "1.5*2^-63": 0x20400000, "FLT_MAX": 0x7F7FFFFF,
+    "denormal": 0x00012345, "inf": 0x7F800000,
+}
+
+
+@pytest.mark.parametrize("name", list(EVERY_A_B))
+def test_every_encoding_of_a(name):
+    """All 2^32 float32 encodings of a against one fixed b (a carry-taking
+    mantissa, a negative power of two, a value whose products cross both the
+    underflow and the overflow boundary, the largest finite value, a
+    denormal, inf), bit for bit against the C oracle, in chunks of 2^27,
+    stopping at the first chunk that differs."""
+    import torch
+    ub = EVERY_A_B[name]
+    note(f"pam_mul, every encoding of a, b = {name} ({ub:#010x})")
+    chunk = 1 << 27
+    bfull = np.full(chunk, ub, dtype=np.uint32).view(np.float32)
+    bd = torch.full((chunk,), np.int32(np.uint32(ub).view(np.int32)), dtype=torch.int32,
+                    device=device()).view(torch.float32)
+    out = torch.empty(chunk, dtype=torch.float32, device=device())
+    for c in range(1 << 5):
+        a = np.arange(c * chunk, (c + 1) * chunk, dtype=np.uint64).astype(np.uint32).view(np.float32)
+        pam.mul(to_dev(a), bd, out=out)
+        got = out.cpu().numpy()
+        want = pam_c.pam_mul(a, bfull)
+        assert_bits_equal(got, want, f"b={name}, a encodings [{c * chunk:#x}, {(c + 1) * chunk:#x})")

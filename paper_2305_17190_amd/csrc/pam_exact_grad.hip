@@ -28,9 +28,10 @@
 //     step each thread adds the general term for its columns whose b is
 //     extreme.
 //   * mod that is normal but not safe: the output's fast-path sum is
-//     discarded; up to two such outputs per thread keep their own
-//     accumulator, summed over every k with the general term.  A workgroup
-//     with a thread holding more takes the general term for every term.
+//     discarded; the workgroup lists such outputs in LDS (up to 512 of the
+//     tile's 16384) and deals them out evenly over its threads, each keeping
+//     the sums of at most two, over every k with the general term.  A tile
+//     with more takes the general term for every term.
 //   * zero / denormal mod: the output is zero.
 // The general term needs mod's exponent field, kept for the whole tile in
 // LDS as bytes; mod's mantissa stays in registers for the fast path.
@@ -170,9 +171,11 @@ pam_exact_grad_kernel(GemmParams p) {
     constexpr int LDE = BN / 4 + 1;   // words per row of the Mod exponent bytes
     __shared__ __attribute__((aligned(16))) uint32_t sA[BK][LDA];
     __shared__ __attribute__((aligned(16))) uint32_t sB[2][BK][LDB];
+    constexpr int kListCap = 2 * NT;   // extreme-Mod outputs a tile lists
     __shared__ uint32_t sE[BM][LDE];   // Mod exponent fields, four columns per word
     __shared__ uint32_t sSlow[2];      // [chunk parity] steps holding an extreme b
-    __shared__ uint32_t sDense;        // some thread has more than two extreme-Mod outputs
+    __shared__ uint32_t sCount;        // extreme-Mod outputs of the tile
+    __shared__ uint32_t sList[2][kListCap];   // their (row << 16 | column) and Mod words
 
     const int tid = threadIdx.x;
     const int tx = tid % TXN;
@@ -202,17 +205,13 @@ pam_exact_grad_kernel(GemmParams p) {
     if (tid < 2)
         sSlow[tid] = 0u;
     if (tid == 0)
-        sDense = 0u;
+        sCount = 0u;
     __syncthreads();
 
     // The micro-tile's Mod mantissas, fixed for the whole K loop, and its
-    // exponent fields in LDS; up to two outputs with an extreme Mod keep
-    // their own accumulator (row, column and Mod word).
+    // exponent fields in LDS; outputs with an extreme Mod go to the tile's
+    // list.
     uint32_t mm[8][8];
-    int nside = 0;
-    uint32_t side_rc[2] = {0u, 0u};
-    uint32_t side_mod[2] = {0u, 0u};
-    float side_acc[2] = {0.0f, 0.0f};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int lr = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
@@ -233,22 +232,16 @@ pam_exact_grad_kernel(GemmParams p) {
                 asm volatile("v_and_b32 %0, 0x7fffff, %1" : "=v"(mm[i][j]) : "v"(u));
                 fields |= ((u >> 23) & 0xFFu) << (8 * jj);
                 if (extreme(u)) {
-                    const uint32_t rc = ((uint32_t)lr << 16) | (uint32_t)lc;
-                    if (nside == 0) {
-                        side_rc[0] = rc;
-                        side_mod[0] = u;
-                    } else {
-                        side_rc[1] = rc;
-                        side_mod[1] = u;
+                    const uint32_t e = atomicAdd(&sCount, 1u);
+                    if (e < (uint32_t)kListCap) {
+                        sList[0][e] = ((uint32_t)lr << 16) | (uint32_t)lc;
+                        sList[1][e] = u;
                     }
-                    ++nside;
                 }
             }
             sE[lr][(h == 0 ? tx : HN / 4 + tx)] = fields;
         }
     }
-    if (nside > 2)
-        sDense = 1u;
 
     float acc[8][8];
 #pragma unroll
@@ -262,7 +255,21 @@ pam_exact_grad_kernel(GemmParams p) {
         lb.load(b_base, n0, p.n, kb, ke, vec_b, tid);
     }
     __syncthreads();
-    const bool dense = sDense != 0u;
+    const uint32_t nlist = sCount;
+    const bool dense = nlist > (uint32_t)kListCap;
+    // This thread's list entries: e = s * NT + slot(tid), slots dealt so that
+    // consecutive entries go to different waves.
+    const uint32_t slot = (uint32_t)((tid % 64) * (NT / 64) + tid / 64);
+    uint32_t side_rc[2], side_mod[2];
+    float side_acc[2] = {0.0f, 0.0f};
+    bool side_on[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const uint32_t idx = (uint32_t)e * NT + slot;
+        side_on[e] = !dense && idx < nlist;
+        side_rc[e] = side_on[e] ? sList[0][idx] : 0u;
+        side_mod[e] = side_on[e] ? sList[1][idx] : 0u;
+    }
 
     for (int c = 0; c < nchunks; ++c) {
         __syncthreads();   // every wave is done reading the previous chunk
@@ -314,7 +321,7 @@ pam_exact_grad_kernel(GemmParams p) {
         if (!dense) {
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
-                if (e < nside) {
+                if (side_on[e]) {
                     const int lr = (int)(side_rc[e] >> 16);
                     const int lc = (int)(side_rc[e] & 0xFFFFu);
 #pragma unroll 4
@@ -345,17 +352,18 @@ pam_exact_grad_kernel(GemmParams p) {
         for (int j = 0; j < 8; ++j) {
             const int col = n0 + (j < 4 ? tx * 4 + j : HN + tx * 4 + (j - 4));
             if (col < p.n) {
-                const bool zero_mod = (__float_as_uint(mrow[col]) & kExpMask) == 0u;
-                orow[col] = zero_mod ? 0.0f : acc[i][j];
+                const uint32_t mu = __float_as_uint(mrow[col]);
+                const bool zero_mod = (mu & kExpMask) == 0u;
+                // extreme-Mod outputs are written by the owner of their list entry
+                if (dense || !extreme(mu))
+                    orow[col] = zero_mod ? 0.0f : acc[i][j];
             }
         }
     }
-    // The extreme-Mod outputs' own sums replace what was just written (same
-    // thread, same address, later in program order).
     if (!dense) {
 #pragma unroll
         for (int e = 0; e < 2; ++e) {
-            if (e < nside) {
+            if (side_on[e]) {
                 const int row = m0 + (int)(side_rc[e] >> 16);
                 const int col = n0 + (int)(side_rc[e] & 0xFFFFu);
                 if (row < p.m && col < p.n)

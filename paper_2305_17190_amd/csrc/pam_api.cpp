@@ -7,6 +7,7 @@
 #include <hsa/hsa_ext_amd.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -56,35 +57,40 @@ struct Shape {
 // 128 x 128 and 128 x 64 tiles with one k-group; 128 x 64 tiles whose two
 // k-groups split each chunk's k steps, and 64 x 64 tiles with one or four
 // (more waves without partial sums in HBM: the groups add their partial
-// tiles in LDS, at more staging work per MAC).  The 128 x 128 tile holds
-// three waves per SIMD, the others two.
-const Shape kShapes[] = {{128, 128, 1, 4, 3, 26.83e12},
-                         {128, 64, 1, 2, 4, 22.15e12},
-                         {128, 64, 2, 4, 2, 20.5e12},
-                         {64, 64, 1, 1, 8, 20.64e12},
-                         {64, 64, 4, 4, 2, 17.39e12}};
+// tiles in LDS, at more staging work per MAC).  Resident workgroups per
+// compute unit follow from the float32 kernel's registers and LDS: the
+// 128 x 128 tile holds four waves per SIMD, the 128 x 64 tiles three, the
+// 64 x 64 tiles two.
+const Shape kShapes[] = {{128, 128, 1, 4, 4, 27.55e12},
+                         {128, 64, 1, 2, 6, 23.69e12},
+                         {128, 64, 2, 4, 3, 24.51e12},
+                         {64, 64, 1, 1, 8, 20.31e12},
+                         {64, 64, 4, 4, 2, 20.71e12}};
 constexpr int kComputeUnits = 256;
 constexpr int kSimdsPerCu = 4;
-// Vector-ALU throughput of one SIMD holding 0..3 waves of this kernel,
-// relative to three: one wave issues alone, two pair their adds and fmas
+// Vector-ALU throughput of one SIMD holding 0..4 waves of this kernel,
+// relative to four: one wave issues alone, two pair their adds and fmas
 // but leave barrier and LDS waits exposed.
-constexpr double kSimdEfficiency[4] = {0.0, 0.4161, 0.8558, 1.0};
-constexpr double kWorkgroupFixedS = 5.6e-6;  // first loads, epilogue stores
-constexpr double kSplitFixedS = 6.8e-6;      // second launch, workspace
+constexpr double kSimdEfficiency[5] = {0.0, 0.4495, 0.8693, 0.8743, 1.0};
+constexpr double kWorkgroupFixedS = 3.15e-6;  // first loads, epilogue stores
+constexpr double kSplitFixedS = 12.7e-6;      // second launch, workspace
 // Effective rate of writing and re-reading partial sums: up to a few hundred
 // MB they largely stay in the last-level cache, so above the HBM rate.
-constexpr double kPartialBytesPerS = 10.6e12;
+constexpr double kPartialBytesPerS = 24.7e12;
 // Workgroups start as soon as slots free up, so a partial last round costs
 // less than a full one the more rounds precede it (they end staggered).
-constexpr double kTailDamping = 0.4778;
+constexpr double kTailDamping = 0.925;
 // Compute units run at different clocks under load, so the last round of
-// workgroups does not end at once: the launch ends this fraction of one
-// workgroup's duration after the average, scaled by how many slots the last
-// round leaves without a shorter partial-round workgroup to absorb it.
-constexpr double kRoundImbalance = 0.078;
+// workgroups does not end at once: the launch ends a fraction of the last
+// workgroups' duration after the average, scaled by how many slots the last
+// round leaves without a shorter partial-round workgroup to absorb it.  A
+// round that started together (the first) ends closer together than one
+// whose workgroups started staggered behind earlier rounds.
+constexpr double kRoundImbalance = 0.0408;
+constexpr double kStaggeredImbalance = 0.1415;
 // Split-K plans must beat the best unsplit plan by this factor (they change
 // the summation order and take a workspace).
-constexpr double kSplitMargin = 0.97;
+constexpr double kSplitMargin = 0.98;
 // Plans with whole-K tiles beside split ones run in one launch; the planner
 // offers them up to this many tiles.
 constexpr int64_t kMaxHybridTiles = 1 << 20;
@@ -94,7 +100,7 @@ constexpr int kSplitChoices[] = {1, 2, 3, 4, 5, 6, 7, 8, 12, 16, 24, 32, 48, 56,
 double cu_efficiency(int waves_per_cu) {
     const int base = waves_per_cu / kSimdsPerCu;
     const int extra = waves_per_cu % kSimdsPerCu;
-    return (extra * kSimdEfficiency[std::min(base + 1, 3)] + (kSimdsPerCu - extra) * kSimdEfficiency[std::min(base, 3)]) /
+    return (extra * kSimdEfficiency[std::min(base + 1, 4)] + (kSimdsPerCu - extra) * kSimdEfficiency[std::min(base, 4)]) /
            kSimdsPerCu;
 }
 
@@ -125,14 +131,17 @@ double rounds_time(const Shape &c, int64_t wgs, double wg_s, int64_t before) {
         const double even = wg_s * double(rest) / double(slots);
         t += even + (partial - even) / (1.0 + kTailDamping * double(before + rounds));
     }
-    if (before + rounds > 0)
-        t += kRoundImbalance * wg_s * (1.0 - double(rest) / double(slots));
+    if (before + rounds > 0) {
+        const bool staggered = before + rounds + (rest > 0 ? 1 : 0) > 1;
+        t += (staggered ? kStaggeredImbalance : kRoundImbalance) * wg_s * (1.0 - double(rest) / double(slots));
+    }
     return t;
 }
 
-// Estimated time of a plan: the whole-K tiles (a whole number of rounds in
-// the plans considered), then the K slices of the split tiles, plus for
-// split-K a second launch and the partial sums' round trip through memory.
+// Estimated time of a plan: the whole-K tiles' full rounds, then the K
+// slices of the split tiles together with the whole-K tiles of a partial
+// round (counted as the slices they displace), plus for split-K a second
+// launch and the partial sums' round trip through memory.
 double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t k, int64_t batch) {
     const int64_t bk = pamk::kChunkK * c.kw;
     const int64_t slots = (int64_t)c.per_cu * kComputeUnits;
@@ -144,8 +153,10 @@ double plan_time(const Shape &c, const Plan &p, int64_t m, int64_t n, int64_t k,
     const int64_t whole = std::min(p.whole_tiles, tiles);
     const int64_t split_tiles = tiles - whole;
     const int64_t before = whole / slots;
+    const int64_t rem = whole % slots;
     const double wg_slice = per_chunk * double(ceil_div(p.k_per_split, bk)) + kWorkgroupFixedS;
-    double t = double(before) * wg_whole + rounds_time(c, split_tiles * p.splits, wg_slice, before);
+    const int64_t displaced = rem > 0 ? (int64_t)std::ceil(double(rem) * wg_whole / wg_slice) : 0;
+    double t = double(before) * wg_whole + rounds_time(c, split_tiles * p.splits + displaced, wg_slice, before);
     t += kSplitFixedS + double(p.splits + 1) * double(split_tiles) * c.bm * c.bn * 4.0 / kPartialBytesPerS;
     return t;
 }
@@ -204,10 +215,14 @@ constexpr size_t kAnyWorkspace = ~(size_t)0;
 
 // The cheapest plan by plan_time whose split-K partial sums fit in
 // max_ws_bytes (0: no split-K): for each tile shape every split count
-// (slices of at least four chunks), and, when the tiles leave a partial last
-// round, split counts for just that round's tiles (or those of the last
-// round and a half) while the rest take the whole K.  A plan with split-K
-// must beat the best unsplit one by kSplitMargin.
+// (slices of at least four chunks), and, for the one-k-group tiles, hybrid
+// plans that split only the last tiles (those of a partial last round, of
+// the last round and that one, or a quarter or half of a round's slots)
+// while the rest take the whole K.  A hybrid's slices are short, at least
+// four per tile and about one per 20 chunks up to 16: the launch then ends
+// on short workgroups (measured: fewer, longer slices end later than the
+// model's imbalance term predicts).  A plan with split-K must beat the best
+// unsplit one by kSplitMargin.
 Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch, size_t max_ws_bytes) {
     double best_t[2] = {0.0, 0.0};
     Plan best[2] = {};
@@ -232,16 +247,20 @@ Plan choose_plan(int64_t m, int64_t n, int64_t k, int64_t batch, size_t max_ws_b
         const int64_t slots = (int64_t)c.per_cu * kComputeUnits;
         const int64_t tiles = ceil_div(m, c.bm) * ceil_div(n, c.bn) * batch;
         const int64_t rest = tiles % slots;
+        const int64_t hybrid_min = std::max<int64_t>(4, std::min<int64_t>(16, ceil_div(k, pamk::kChunkK) / 20));
         for (const int s : kSplitChoices) {
             if (s > most)
                 break;
             consider(c, make_plan(c, k, s));
-            if (s == 1 || rest == 0 || tiles <= slots)
+            if (s < hybrid_min || c.kw != 1 || tiles > kMaxHybridTiles)
                 continue;
-            for (const int64_t tail : {rest, rest + slots}) {
-                if (tail >= tiles || tiles > kMaxHybridTiles)
-                    continue;
-                consider(c, make_plan(c, k, s, tiles - tail));
+            const int64_t tails[4] = {rest, rest + slots, slots / 4, slots / 2};
+            for (int i = 0; i < 4; ++i) {
+                bool seen = false;
+                for (int j = 0; j < i; ++j)
+                    seen = seen || tails[j] == tails[i];
+                if (!seen && tails[i] > 0 && tails[i] < tiles)
+                    consider(c, make_plan(c, k, s, tiles - tails[i]));
             }
         }
     }

@@ -1,0 +1,672 @@
+// PAM matrix product for float32 operands with the operand chunks copied
+// from global memory straight into LDS (gfx950's global_load_lds_dwordx4).
+//
+// Same tiles, work items, k-groups, step paths (S1 / S2 / S3 / SPECIAL) and
+// summation order as pam_gemm_kernel in pam_kernels.hip, so both give the
+// same bits; what differs is the staging:
+//
+// * Each chunk's operand segments (16 bytes: four elements consecutive in
+//   memory) are copied by the memory pipeline into an LDS landing buffer.
+//   No register holds a chunk while its copy is in flight, so the kernel
+//   keeps only the accumulators and the compute step's operands live across
+//   the K loop, and the 128 x 128 tile fits four waves per SIMD instead of
+//   three.
+// * At the chunk boundary each thread re-reads the segments it copied (its
+//   own, so no barrier is needed for them), scans and encodes them, and
+//   writes them k-major into the compute buffer.  A thread holds L rows of
+//   one k quad of a K-contiguous operand and writes each k as one L-word
+//   store; the lanes of a wave write consecutive columns of one k row, so
+//   the stores are free of bank conflicts (the register-staged kernel's
+//   word stores to four k rows conflict four ways).
+// * A is kept as its own encoding only (one plane instead of three): the S1
+//   step reads it as it is, and the rarer S2 / S3 steps derive 1 + M_A and
+//   +-2^E_A from it with two bit operations per value.
+// * The chunk after next is copied while a chunk is computed; segments that
+//   cannot be copied whole (the K tail, an unaligned operand, a segment
+//   straddling the last column) are loaded element by element from global
+//   memory when the chunk is encoded.
+//
+// With k-groups (KW > 1) the groups other than the first write their
+// partial tiles to LDS, and the first group adds them in group order and
+// stores the tile.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pam_internal.h"
+#include "pam_scalar.h"
+
+namespace pamk {
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One micro-tile row of an S2 or S3 step from A's own encoding a: first
+// 1 + M_A (exponent field 127, a's mantissa) and +-2^E_A (a with its mantissa
+// cleared, +-0 for zero / denormal a), then the SCALED products with the
+// eight b' values.  S2: acc[j] = fma(aM + b'[j], m, acc[j]); S3: the product
+// rounded on its own (an underflowing product flushes to zero), then added.
+// One asm block per row keeps the derived values' lifetime to the row.
+#define PAM_DMA_ROW_OPERANDS                                                                               \
+    : [am] "=&v"(am), [m] "=&v"(m), [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [t3] "=&v"(t3),       \
+      [t4] "=&v"(t4), [t5] "=&v"(t5), [t6] "=&v"(t6), [t7] "=&v"(t7), [c0] "+v"(acc[0]), [c1] "+v"(acc[1]), \
+      [c2] "+v"(acc[2]), [c3] "+v"(acc[3]), [c4] "+v"(acc[4]), [c5] "+v"(acc[5]), [c6] "+v"(acc[6]),        \
+      [c7] "+v"(acc[7])                                                                                    \
+    : [a] "v"(a), [b0] "v"(bb[0]), [b1] "v"(bb[1]), [b2] "v"(bb[2]), [b3] "v"(bb[3]), [b4] "v"(bb[4]),     \
+      [b5] "v"(bb[5]), [b6] "v"(bb[6]), [b7] "v"(bb[7]), [mant] "v"(kMant), [bias] "v"(kBias),              \
+      [se] "v"(kSignExp)
+#define PAM_DMA_ROW_HEAD                                                                                   \
+    "v_and_or_b32 %[am], %[a], %[mant], %[bias]\n\tv_and_b32 %[m], %[a], %[se]\n\t"                        \
+    "v_add_u32 %[t0], %[am], %[b0]\n\tv_add_u32 %[t1], %[am], %[b1]\n\t"                                   \
+    "v_add_u32 %[t2], %[am], %[b2]\n\tv_add_u32 %[t3], %[am], %[b3]\n\t"                                   \
+    "v_add_u32 %[t4], %[am], %[b4]\n\tv_add_u32 %[t5], %[am], %[b5]\n\t"                                   \
+    "v_add_u32 %[t6], %[am], %[b6]\n\tv_add_u32 %[t7], %[am], %[b7]\n\t"
+
+__device__ __forceinline__ void dma_s2_row(float (&acc)[8], uint32_t a, const uint32_t (&bb)[8]) {
+    uint32_t am, m, t0, t1, t2, t3, t4, t5, t6, t7;
+    asm(PAM_DMA_ROW_HEAD
+        "v_fmac_f32 %[c0], %[t0], %[m]\n\tv_fmac_f32 %[c1], %[t1], %[m]\n\t"
+        "v_fmac_f32 %[c2], %[t2], %[m]\n\tv_fmac_f32 %[c3], %[t3], %[m]\n\t"
+        "v_fmac_f32 %[c4], %[t4], %[m]\n\tv_fmac_f32 %[c5], %[t5], %[m]\n\t"
+        "v_fmac_f32 %[c6], %[t6], %[m]\n\tv_fmac_f32 %[c7], %[t7], %[m]"
+        PAM_DMA_ROW_OPERANDS);
+}
+
+__device__ __forceinline__ void dma_s3_row(float (&acc)[8], uint32_t a, const uint32_t (&bb)[8]) {
+    uint32_t am, m, t0, t1, t2, t3, t4, t5, t6, t7;
+    asm(PAM_DMA_ROW_HEAD
+        "v_mul_f32 %[t0], %[t0], %[m]\n\tv_mul_f32 %[t1], %[t1], %[m]\n\t"
+        "v_mul_f32 %[t2], %[t2], %[m]\n\tv_mul_f32 %[t3], %[t3], %[m]\n\t"
+        "v_mul_f32 %[t4], %[t4], %[m]\n\tv_mul_f32 %[t5], %[t5], %[m]\n\t"
+        "v_mul_f32 %[t6], %[t6], %[m]\n\tv_mul_f32 %[t7], %[t7], %[m]\n\t"
+        "v_add_f32 %[c0], %[c0], %[t0]\n\tv_add_f32 %[c1], %[c1], %[t1]\n\t"
+        "v_add_f32 %[c2], %[c2], %[t2]\n\tv_add_f32 %[c3], %[c3], %[t3]\n\t"
+        "v_add_f32 %[c4], %[c4], %[t4]\n\tv_add_f32 %[c5], %[c5], %[t5]\n\t"
+        "v_add_f32 %[c6], %[c6], %[t6]\n\tv_add_f32 %[c7], %[c7], %[t7]"
+        PAM_DMA_ROW_OPERANDS);
+}
+#undef PAM_DMA_ROW_HEAD
+#undef PAM_DMA_ROW_OPERANDS
+
+// A whole S1 step (acc[i][j] += a_i + b'_j for the 8 x 8 micro-tile) as one
+// instruction sequence.
+#define PAM_DMA_S1_ROW(R, A)                                                                               \
+    "v_add_u32 %[t0], %[" #A "], %[b0]\n\tv_add_u32 %[t1], %[" #A "], %[b1]\n\t"                           \
+    "v_add_u32 %[t2], %[" #A "], %[b2]\n\tv_add_u32 %[t3], %[" #A "], %[b3]\n\t"                           \
+    "v_add_u32 %[t4], %[" #A "], %[b4]\n\tv_add_u32 %[t5], %[" #A "], %[b5]\n\t"                           \
+    "v_add_u32 %[t6], %[" #A "], %[b6]\n\tv_add_u32 %[t7], %[" #A "], %[b7]\n\t"                           \
+    "v_add_f32 %[c" #R "0], %[c" #R "0], %[t0]\n\tv_add_f32 %[c" #R "1], %[c" #R "1], %[t1]\n\t"           \
+    "v_add_f32 %[c" #R "2], %[c" #R "2], %[t2]\n\tv_add_f32 %[c" #R "3], %[c" #R "3], %[t3]\n\t"           \
+    "v_add_f32 %[c" #R "4], %[c" #R "4], %[t4]\n\tv_add_f32 %[c" #R "5], %[c" #R "5], %[t5]\n\t"           \
+    "v_add_f32 %[c" #R "6], %[c" #R "6], %[t6]\n\tv_add_f32 %[c" #R "7], %[c" #R "7], %[t7]\n\t"
+#define PAM_DMA_ACC_ROW(R)                                                                                 \
+    [c##R##0] "+v"(acc[R][0]), [c##R##1] "+v"(acc[R][1]), [c##R##2] "+v"(acc[R][2]),                       \
+        [c##R##3] "+v"(acc[R][3]), [c##R##4] "+v"(acc[R][4]), [c##R##5] "+v"(acc[R][5]),                   \
+        [c##R##6] "+v"(acc[R][6]), [c##R##7] "+v"(acc[R][7])
+
+__device__ __forceinline__ void dma_s1_step(float (&acc)[8][8], const uint4 &al, const uint4 &ah,
+                                            const uint32_t (&bb)[8]) {
+    uint32_t t0, t1, t2, t3, t4, t5, t6, t7;
+    asm(PAM_DMA_S1_ROW(0, a0) PAM_DMA_S1_ROW(1, a1) PAM_DMA_S1_ROW(2, a2) PAM_DMA_S1_ROW(3, a3)
+            PAM_DMA_S1_ROW(4, a4) PAM_DMA_S1_ROW(5, a5) PAM_DMA_S1_ROW(6, a6) PAM_DMA_S1_ROW(7, a7)
+        : PAM_DMA_ACC_ROW(0), PAM_DMA_ACC_ROW(1), PAM_DMA_ACC_ROW(2), PAM_DMA_ACC_ROW(3), PAM_DMA_ACC_ROW(4),
+          PAM_DMA_ACC_ROW(5), PAM_DMA_ACC_ROW(6), PAM_DMA_ACC_ROW(7), [t0] "=&v"(t0), [t1] "=&v"(t1),
+          [t2] "=&v"(t2), [t3] "=&v"(t3), [t4] "=&v"(t4), [t5] "=&v"(t5), [t6] "=&v"(t6), [t7] "=&v"(t7)
+        : [a0] "v"(al.x), [a1] "v"(al.y), [a2] "v"(al.z), [a3] "v"(al.w), [a4] "v"(ah.x), [a5] "v"(ah.y),
+          [a6] "v"(ah.z), [a7] "v"(ah.w), [b0] "v"(bb[0]), [b1] "v"(bb[1]), [b2] "v"(bb[2]), [b3] "v"(bb[3]),
+          [b4] "v"(bb[4]), [b5] "v"(bb[5]), [b6] "v"(bb[6]), [b7] "v"(bb[7]));
+}
+#undef PAM_DMA_S1_ROW
+#undef PAM_DMA_ACC_ROW
+
+// Eight values of one k row of a compute buffer: four at p, four at p + half.
+__device__ __forceinline__ void dma_frag(const uint32_t *p, int half, uint32_t (&out)[8]) {
+    const uint4 lo = *reinterpret_cast<const uint4 *>(p);
+    const uint4 hi = *reinterpret_cast<const uint4 *>(p + half);
+    out[0] = lo.x; out[1] = lo.y; out[2] = lo.z; out[3] = lo.w;
+    out[4] = hi.x; out[5] = hi.y; out[6] = hi.z; out[7] = hi.w;
+}
+
+// One operand's D x BK chunk (D = rows of op(A) or columns of op(B)) in
+// 16-byte segments of four elements consecutive in memory.
+//
+// KCONTIG: a segment is (row o, k quad).  Thread t copies the L rows
+// j * L .. j * L + L - 1 of one k quad kq, so that it can write each k of them
+// as one L-word LDS store.  Lane 16 * q + i of a wave takes row group
+// j = 16 * (wave / (BK / 16)) + i and k quad kq = q + 4 * (wave % (BK / 16)):
+// one copy instruction reads 16 rows x 64 contiguous bytes (16 cache lines,
+// as many as the register-staged loads), and the 16 lanes of each store pass
+// write 16 consecutive row groups of one k row (no bank conflicts).
+//
+// Otherwise a segment is (k, column quad); thread t's segment r is number
+// t + r * NT, so consecutive lanes hold consecutive column quads of one k.
+template <int D, int BK, int NT, bool KCONTIG>
+struct DmaTile {
+    static constexpr int SEGS = D * BK / 4;
+    static constexpr int L = SEGS / NT;                  // segments per thread
+    static constexpr int G = D / L;                      // KCONTIG: row groups
+    static constexpr int KS = BK / 16;                   // KCONTIG: waves per 16 row groups
+    static constexpr int NW = NT / 64;
+    static_assert(L * NT == SEGS && (L == 2 || L == 4), "chunk does not divide over the threads");
+    static_assert(!KCONTIG || (G % 16 == 0 && BK % 16 == 0 && (G / 16) * KS == NW), "bad K-contiguous segment split");
+
+    uint4 v[L];          // the segments being encoded (live only at the chunk boundary)
+
+    static __device__ __forceinline__ int seg_o(int t, int r) {
+        return KCONTIG ? (16 * ((t >> 6) / KS) + (t & 15)) * L + r : ((t + r * NT) % (D / 4)) * 4;
+    }
+    static __device__ __forceinline__ int seg_k(int t, int r) {
+        return KCONTIG ? (((t & 63) >> 4) + 4 * ((t >> 6) % KS)) * 4 : (t + r * NT) / (D / 4);
+    }
+
+    // Byte offset of segment r from its chunk's base.  Rows past o_lim are
+    // clamped to the last valid row (their outputs are discarded); a segment
+    // straddling the last valid column is not copied (copyable) and is
+    // loaded element by element.  Recomputed per chunk from the thread
+    // index, so that no per-thread offsets stay live across the K loop.
+    static __device__ __forceinline__ uint32_t boff(int tid, int r, int64_t ld, int o0, int o_lim) {
+        const int o = seg_o(tid, r);
+        const int kk = seg_k(tid, r);
+        if (KCONTIG)
+            return (uint32_t)(((int64_t)(min(o0 + o, o_lim - 1) - o0) * ld + kk) * 4);
+        return (uint32_t)(((int64_t)kk * ld + o) * 4);
+    }
+    static __device__ __forceinline__ bool copyable(int tid, int r, int o0, int o_lim) {
+        return KCONTIG || o0 + seg_o(tid, r) + 3 < o_lim;
+    }
+
+    // LDS landing slot of segment r of this thread (wave w, lane): block
+    // (r * NW + w) of 64 segments, the lane's 16 bytes within it.
+    static __device__ __forceinline__ uint32_t *slot_block(uint32_t *raw, int r, int w) {
+        return raw + (r * NW + w) * 256;
+    }
+
+    // Start copying the chunk at `base` into the landing buffer.  Called only
+    // for an interior chunk of an aligned operand.
+    static __device__ __forceinline__ void copy(const float *__restrict__ base, uint32_t *raw, int w, int tid,
+                                                int64_t ld, int o0, int o_lim) {
+        const char *cb = reinterpret_cast<const char *>(base);
+#pragma unroll
+        for (int r = 0; r < L; ++r) {
+            if (copyable(tid, r, o0, o_lim))
+                __builtin_amdgcn_global_load_lds((const void *)(cb + boff(tid, r, ld, o0, o_lim)),
+                                                 (lds_void_t *)slot_block(raw, r, w), 16, 0, 0);
+        }
+    }
+
+    // The thread's segments of chunk [k0, k0 + BK): from the landing buffer
+    // when they were copied, else element by element from global memory
+    // (elements at k >= k_lim are zero).
+    __device__ __forceinline__ void fetch(const uint32_t *raw, int w, int lane, bool copied,
+                                          const float *__restrict__ base, int64_t ld, int o0, int o_lim, int k0,
+                                          int k_lim, int tid) {
+#pragma unroll
+        for (int r = 0; r < L; ++r) {
+            if (copied && copyable(tid, r, o0, o_lim))
+                v[r] = *reinterpret_cast<const uint4 *>(slot_block(const_cast<uint32_t *>(raw), r, w) + lane * 4);
+            else
+                v[r] = load_elements(reinterpret_cast<const char *>(base), r, ld, o0, o_lim, k0, k_lim, tid);
+        }
+    }
+
+    static __device__ __forceinline__ uint4 load_elements(const char *cb, int r, int64_t ld, int o0, int o_lim,
+                                                          int k0, int k_lim, int tid) {
+        const float *src = reinterpret_cast<const float *>(cb + boff(tid, r, ld, o0, o_lim));
+        const int kk = seg_k(tid, r);
+        uint32_t e[4];
+        if (KCONTIG) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                e[c] = (k0 + kk + c < k_lim) ? __float_as_uint(src[c]) : 0u;
+        } else {
+            const int o = seg_o(tid, r);
+            const float *row = src - o;
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                e[c] = (k0 + kk < k_lim) ? __float_as_uint(row[min(o0 + o + c, o_lim - 1) - o0]) : 0u;
+        }
+        return make_uint4(e[0], e[1], e[2], e[3]);
+    }
+
+    // Round every held element to 23 - drop mantissa bits, nearest even (inf
+    // and NaN unchanged).
+    __device__ __forceinline__ void round_mantissa(int drop) {
+        const uint32_t low = (1u << drop) - 1u;
+        const uint32_t half_m1 = low >> 1;
+#pragma unroll
+        for (int r = 0; r < L; ++r) {
+            uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t u = e[c];
+                const uint32_t rounded = (u + half_m1 + ((u >> drop) & 1u)) & ~low;
+                e[c] = ((u & kExpMask) == kExpMask) ? u : rounded;
+            }
+            v[r] = make_uint4(e[0], e[1], e[2], e[3]);
+        }
+    }
+
+    // Bit 0: some element has exponent field below 64; bit 1: some element
+    // needs the SPECIAL path (inf, NaN, |x| >= 2^64); bit 2 + r: segment r
+    // holds an element of the first kind.
+    __device__ __forceinline__ uint32_t scan() const {
+        uint32_t hi = 0, groups = 0;
+#pragma unroll
+        for (int r = 0; r < L; ++r) {
+            const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+            uint32_t lo = 0xFFFFFFFFu;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const uint32_t ex = e[c] & kExpMask;
+                hi = max(hi, ex);
+                lo = min(lo, ex);
+            }
+            if (lo < (64u << 23))
+                groups |= 1u << r;
+        }
+        return (groups != 0u ? 1u : 0u) | (hi >= (191u << 23) ? 2u : 0u) | (groups << 2);
+    }
+
+    // Element encodings: A as it is; B as b' = b - bias after flushing a
+    // denormal b to its signed zero (multiplying by 1.0 flushes it; NaN stays
+    // NaN).
+    static __device__ __forceinline__ uint32_t enc(uint32_t u, bool is_b) {
+        if (!is_b)
+            return u;
+        uint32_t f;
+        asm("v_mul_f32 %0, 1.0, %1" : "=v"(f) : "v"(u));
+        return f - kBias;
+    }
+
+    // Write the encoded chunk k-major into s[k * D + o] and mark the step
+    // masks (as the register-staged kernel's TileLoader::store).
+    template <typename SlotOf>
+    __device__ __forceinline__ void store(uint32_t *s, bool is_b, int tid, uint32_t low_groups, uint32_t *mask,
+                                          int slots, SlotOf slot_of) const {
+        if (KCONTIG) {
+            const int o0 = seg_o(tid, 0);
+            const int k0 = seg_k(tid, 0);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                uint32_t w[L];
+#pragma unroll
+                for (int r = 0; r < L; ++r) {
+                    const uint32_t u = c == 0 ? v[r].x : c == 1 ? v[r].y : c == 2 ? v[r].z : v[r].w;
+                    w[r] = enc(u, is_b);
+                }
+                uint32_t *dst = s + (k0 + c) * D + o0;
+                if constexpr (L == 2)
+                    *reinterpret_cast<uint2 *>(dst) = make_uint2(w[0], w[1]);
+                else
+                    *reinterpret_cast<uint4 *>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < L; ++r) {
+                const int o = seg_o(tid, r);
+                const int kk = seg_k(tid, r);
+                *reinterpret_cast<uint4 *>(s + kk * D + o) =
+                    make_uint4(enc(v[r].x, is_b), enc(v[r].y, is_b), enc(v[r].z, is_b), enc(v[r].w, is_b));
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < L; ++r) {
+            // Rare: the wave skips this unless one of its lanes holds such an
+            // element in segment r.
+            if ((low_groups >> r) & 1u) {
+                const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+                const int o = seg_o(tid, r);
+                const int kk = seg_k(tid, r);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t ex = e[c] & kExpMask;
+                    if (ex < (64u << 23)) {
+                        const int k = KCONTIG ? kk + c : kk;
+                        const uint32_t bit = 1u << (k % 16);
+                        atomicOr(&mask[(k / 16) * slots + slot_of(KCONTIG ? o : o + c)],
+                                 ex != 0u ? (bit | (bit << 16)) : bit);
+                    }
+                }
+            }
+        }
+    }
+};
+
+// Waves per SIMD the tile is compiled for (registers per wave 512 / waves),
+// matching what its LDS footprint allows on a 160 KB compute unit.
+constexpr int dma_waves_per_simd(int bm, int bn, int kw) {
+    return (bm == 128 && bn == 128 && kw == 1) ? 4 : (bm == 128 && bn == 64) ? 3 : 2;
+}
+
+template <int BM, int BN, int KW, bool TA, bool TB>
+__global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(dma_waves_per_simd(BM, BN, KW))))
+pam_gemm_dma_kernel(GemmParams p) {
+    constexpr int KPG = kChunkK;           // k steps per group per chunk
+    constexpr int BK = KPG * KW;
+    constexpr int NTG = BM * BN / 64;
+    constexpr int NT = NTG * KW;
+    constexpr int NW = NT / 64;
+    constexpr int NRW = NTG / 64;
+    constexpr int WC = BN / 64;
+    constexpr int WR = NRW / WC;
+    constexpr int NSLOT = WR + WC;
+    static_assert(WC >= 1 && WR * WC == NRW && BM / 64 == WR, "waves do not tile the output tile");
+    constexpr int HM = BM / 2;
+    constexpr int HN = BN / 2;
+    constexpr int LDR = BN + 4;            // partial-tile rows (KW > 1)
+    using TileA = DmaTile<BM, BK, NT, !TA>;
+    using TileB = DmaTile<BN, BK, NT, TB>;
+    constexpr int kRawA = TileA::SEGS * 4;
+    constexpr int kRawB = TileB::SEGS * 4;
+    constexpr int kStage = kRawA + kRawB + BK * BM + BK * BN;
+    constexpr int kRed = (KW - 1) * BM * LDR;
+    // Landing buffers, then the k-major compute buffers; for KW > 1 the
+    // partial tiles reuse the same bytes after the K loop.
+    __shared__ __attribute__((aligned(16))) uint32_t smem[kStage > kRed ? kStage : kRed];
+    __shared__ uint32_t sVote[NW];
+    __shared__ uint32_t sMask[2][KW * NSLOT];
+    uint32_t *rawA = smem;
+    uint32_t *rawB = smem + kRawA;
+    uint32_t *encA = smem + kRawA + kRawB;
+    uint32_t *encB = encA + BK * BM;
+
+    const int tid = threadIdx.x;
+    const int grp = tid / NTG;
+    const int t = tid % NTG;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int gwave = t >> 6;
+    const int wr = gwave / WC;
+    const int wc = gwave % WC;
+    const int lane = tid & 63;
+    const int tx = wc * 8 + (lane & 7);
+    const int ty = wr * 8 + (lane >> 3);
+    const uint32_t item = blockIdx.x;
+    const bool whole = item < (uint32_t)p.whole;
+    const uint32_t rel = item - (uint32_t)p.whole;
+    const uint32_t nsplit = (uint32_t)max(p.split_tiles, 1);
+    const uint32_t st = whole ? 0u : rel % nsplit;
+    const int split = whole ? 0 : (int)(rel / nsplit);
+    const uint32_t tile_lin = whole ? item : (uint32_t)p.whole + st;
+    const int64_t bz = tile_lin / (uint32_t)p.tiles;
+    const int tile = (int)(tile_lin % (uint32_t)p.tiles);
+    const int tm = tile / p.tiles_n;
+    const int tn = tile % p.tiles_n;
+    const int m0 = tm * BM;
+    const int n0 = tn * BN;
+    const int kb = whole ? 0 : split * p.k_per_split;
+    const int ke = whole ? p.k : min(p.k, kb + p.k_per_split);
+    const int nchunks = ke > kb ? (ke - kb + BK - 1) / BK : 0;
+
+    const float *a_base = p.A + bz * p.strideA + (TA ? (int64_t)kb * p.lda + m0 : (int64_t)m0 * p.lda + kb);
+    const float *b_base = p.B + bz * p.strideB + (TB ? (int64_t)n0 * p.ldb + kb : (int64_t)kb * p.ldb + n0);
+    const int64_t a_step = TA ? (int64_t)BK * p.lda : BK;
+    const int64_t b_step = TB ? BK : (int64_t)BK * p.ldb;
+    const bool vec_a = p.vec_a != 0;
+    const bool vec_b = p.vec_b != 0;
+
+    TileA la;
+    TileB lb;
+    auto a_slot = [](int o) { return ((o % HM) / 4) / 8; };
+    auto b_slot = [](int o) { return WR + ((o % HN) / 4) / 8; };
+
+    float acc[8][8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            acc[i][j] = 0.0f;
+
+    if (tid < 2 * KW * NSLOT)
+        (&sMask[0][0])[tid] = 0u;
+
+    // Chunk c is copied when it is whole (k0 + BK <= ke) and its operand
+    // aligned.
+    if (nchunks > 0 && kb + BK <= ke) {
+        if (vec_a)
+            TileA::copy(a_base, rawA, wave, tid, p.lda, m0, p.m);
+        if (vec_b)
+            TileB::copy(b_base, rawB, wave, tid, p.ldb, n0, p.n);
+    }
+
+    const int k_first = grp * KPG;
+    for (int c = 0; c < nchunks; ++c) {
+        const int k0 = kb + c * BK;
+        const bool interior = k0 + BK <= ke;
+        // The thread index through an empty asm: staging addresses derived
+        // from it are recomputed per chunk instead of being hoisted out of
+        // the loop into registers that would stay live during the steps.
+        int tid_c = tid;
+        asm volatile("" : "+v"(tid_c));
+        __builtin_amdgcn_s_setprio(1);
+        // This thread's copies of chunk c have landed (the only vector-memory
+        // operations outstanding).
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        la.fetch(rawA, wave, tid_c & 63, interior && vec_a, a_base + c * a_step, p.lda, m0, p.m, k0, ke, tid_c);
+        lb.fetch(rawB, wave, tid_c & 63, interior && vec_b, b_base + c * b_step, p.ldb, n0, p.n, k0, ke, tid_c);
+
+        if (p.round_drop != 0) {
+            la.round_mantissa(p.round_drop);
+            lb.round_mantissa(p.round_drop);
+        }
+        const uint32_t fa = la.scan();
+        const uint32_t fb = lb.scan();
+        const uint64_t sp = __ballot((fa | fb) & 2u);
+        uint32_t *mask = sMask[c & 1];
+        __syncthreads();   // every wave is done reading the previous chunk (and zeroing this mask)
+        la.store(encA, false, tid_c, fa >> 2, mask, NSLOT, a_slot);
+        lb.store(encB, true, tid_c, fb >> 2, mask, NSLOT, b_slot);
+        if (lane == 0)
+            sVote[wave] = sp ? 1u : 0u;
+        __syncthreads();
+
+        uint32_t vote = 0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+            vote |= sVote[w];
+        const bool special = vote != 0u;
+        const uint32_t low =
+            __builtin_amdgcn_readfirstlane(mask[grp * NSLOT + wr] | mask[grp * NSLOT + WR + wc]);
+        if (tid < KW * NSLOT)
+            sMask[(c + 1) & 1][tid] = 0u;
+
+        // The next chunk's copies land while this one is computed (the
+        // landing slots are this thread's own and were read above).
+        if (c + 1 < nchunks && k0 + 2 * BK <= ke) {
+            if (vec_a)
+                TileA::copy(a_base + (c + 1) * a_step, rawA, wave, tid_c, p.lda, m0, p.m);
+            if (vec_b)
+                TileB::copy(b_base + (c + 1) * b_step, rawB, wave, tid_c, p.ldb, n0, p.n);
+        }
+
+        __builtin_amdgcn_s_setprio(0);
+
+        const uint32_t s1_bits = special ? 0u : (~low & 0xFFFFu);
+        const uint32_t s2_bits = special ? 0u : (low & ~(low >> 16) & 0xFFFFu);
+        const uint32_t s3_bits = special ? 0u : (low >> 16);
+        const uint32_t sp_bits = special ? 0xFFFFu : 0u;
+        const uint32_t *a_row = encA + k_first * BM + ty * 4;
+        const uint32_t *b_row = encB + k_first * BN + tx * 4;
+        {
+            uint4 al[2], ah[2];
+            uint32_t bq[2][8];
+            auto rd = [&](int k, int slot) {
+                al[slot] = *reinterpret_cast<const uint4 *>(a_row + k * BM);
+                ah[slot] = *reinterpret_cast<const uint4 *>(a_row + k * BM + HM);
+                const uint4 lo = *reinterpret_cast<const uint4 *>(b_row + k * BN);
+                const uint4 hi = *reinterpret_cast<const uint4 *>(b_row + k * BN + HN);
+                bq[slot][0] = lo.x; bq[slot][1] = lo.y; bq[slot][2] = lo.z; bq[slot][3] = lo.w;
+                bq[slot][4] = hi.x; bq[slot][5] = hi.y; bq[slot][6] = hi.z; bq[slot][7] = hi.w;
+            };
+            if (s1_bits != 0u) {
+                rd(0, 0);
+#pragma unroll
+                for (int k = 0; k < 16; ++k) {
+                    const int cur = k & 1;
+                    if (k + 1 < 16)
+                        rd(k + 1, cur ^ 1);
+                    __builtin_amdgcn_sched_barrier(0);
+                    if ((s1_bits >> k) & 1u)
+                        dma_s1_step(acc, al[cur], ah[cur], bq[cur]);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            }
+        }
+        // S2 steps, then S3 steps (1 + M_A and +-2^E_A derived per row).
+        for (uint32_t todo = s2_bits; todo != 0u; todo &= todo - 1u) {
+            const int kk = __builtin_ctz(todo);
+            uint32_t aa[8], bb[8];
+            dma_frag(a_row + kk * BM, HM, aa);
+            dma_frag(b_row + kk * BN, HN, bb);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                dma_s2_row(acc[i], aa[i], bb);
+        }
+        for (uint32_t todo = s3_bits; todo != 0u; todo &= todo - 1u) {
+            const int kk = __builtin_ctz(todo);
+            uint32_t aa[8], bb[8];
+            dma_frag(a_row + kk * BM, HM, aa);
+            dma_frag(b_row + kk * BN, HN, bb);
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                dma_s3_row(acc[i], aa[i], bb);
+        }
+        // SPECIAL: the complete definition per MAC (B: b' + bias, denormals
+        // already zero).
+#pragma unroll 1
+        for (uint32_t todo = sp_bits; todo != 0u; todo &= todo - 1u) {
+            const int kk = __builtin_ctz(todo);
+            uint32_t aa[8], bb[8];
+            dma_frag(a_row + kk * BM, HM, aa);
+            dma_frag(b_row + kk * BN, HN, bb);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    acc[i][j] += __uint_as_float(pam_full(aa[i], bb[j] + kBias));
+            }
+        }
+    }
+
+    // Epilogue: the output tile in C, or this K slice's partial tile (packed,
+    // written whole).
+    float *out;
+    int64_t ld;
+    int lim_m, lim_n;
+    bool vec;
+    if (whole) {
+        out = p.C + bz * p.strideC + (int64_t)m0 * p.ldc + n0;
+        ld = p.ldc;
+        lim_m = p.m - m0;
+        lim_n = p.n - n0;
+        vec = p.vec_c != 0;
+    } else {
+        out = p.W + ((int64_t)split * p.split_tiles + st) * (BM * BN);
+        ld = BN;
+        lim_m = BM;
+        lim_n = BN;
+        vec = true;
+    }
+    if constexpr (KW > 1) {
+        // Groups 1.. write their partial tiles; group 0 adds them, in group
+        // order, to its own.
+        __syncthreads();   // the LDS buffers are free: every wave is past its last chunk
+        float *red = reinterpret_cast<float *>(smem);
+        if (grp > 0) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int col = h == 0 ? tx * 4 : HN + tx * 4;
+                    *reinterpret_cast<float4 *>(&red[((grp - 1) * BM + row) * LDR + col]) =
+                        make_float4(acc[i][4 * h], acc[i][4 * h + 1], acc[i][4 * h + 2], acc[i][4 * h + 3]);
+                }
+            }
+        }
+        __syncthreads();
+        if (grp > 0)
+            return;
+        // Row by row: the row's partial values, then its adds (in inline asm,
+        // in group order, so that the compiler neither loads every partial
+        // tile up front nor moves the adds past the next row's loads).
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            asm volatile("" ::: "memory");
+            const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+#pragma unroll
+            for (int g = 1; g < KW; ++g) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int col = h == 0 ? tx * 4 : HN + tx * 4;
+                    const float4 x = *reinterpret_cast<const float4 *>(&red[((g - 1) * BM + row) * LDR + col]);
+                    asm volatile("v_add_f32 %0, %0, %4\n\tv_add_f32 %1, %1, %5\n\t"
+                                 "v_add_f32 %2, %2, %6\n\tv_add_f32 %3, %3, %7"
+                                 : "+v"(acc[i][4 * h]), "+v"(acc[i][4 * h + 1]), "+v"(acc[i][4 * h + 2]),
+                                   "+v"(acc[i][4 * h + 3])
+                                 : "v"(x.x), "v"(x.y), "v"(x.z), "v"(x.w));
+                }
+            }
+        }
+    }
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+        if (row >= lim_m)
+            continue;
+        float *orow = out + (int64_t)row * ld;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int col = h == 0 ? tx * 4 : HN + tx * 4;
+            if (vec && col + 3 < lim_n) {
+                const f32x4 v = {acc[i][4 * h], acc[i][4 * h + 1], acc[i][4 * h + 2], acc[i][4 * h + 3]};
+                // The final C with the non-temporal hint (written once);
+                // split partial sums without it (the reduce reads them soon).
+                if (whole)
+                    __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(orow + col));
+                else
+                    *reinterpret_cast<f32x4 *>(orow + col) = v;
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (col + j < lim_n)
+                        orow[col + j] = acc[i][4 * h + j];
+            }
+        }
+    }
+}
+
+template <int BM, int BN, int KW>
+static hipError_t launch_dma_tile(bool ta, bool tb, const GemmParams &p, dim3 grid, hipStream_t stream) {
+    const dim3 block(BM * BN / 64 * KW);
+    if (!ta && !tb)
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, false>), grid, block, 0, stream, p);
+    else if (!ta && tb)
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, true>), grid, block, 0, stream, p);
+    else if (ta && !tb)
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, false>), grid, block, 0, stream, p);
+    else
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, true>), grid, block, 0, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_pam_gemm_dma(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, const GemmParams &p,
+                               hipStream_t stream) {
+    const int64_t items = (int64_t)p.whole + (int64_t)p.split_tiles * p.splits;
+    if (items <= 0 || items > kMaxLaunchItems)
+        return hipErrorInvalidValue;
+    const dim3 grid((unsigned)items);
+    if (tile_m == 128 && tile_n == 128 && kgroups == 1)
+        return launch_dma_tile<128, 128, 1>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 128 && tile_n == 64 && kgroups == 1)
+        return launch_dma_tile<128, 64, 1>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 128 && tile_n == 64 && kgroups == 2)
+        return launch_dma_tile<128, 64, 2>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 64 && tile_n == 64 && kgroups == 1)
+        return launch_dma_tile<64, 64, 1>(trans_a, trans_b, p, grid, stream);
+    if (tile_m == 64 && tile_n == 64 && kgroups == 4)
+        return launch_dma_tile<64, 64, 4>(trans_a, trans_b, p, grid, stream);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace pamk

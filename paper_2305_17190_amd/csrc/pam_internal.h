@@ -58,6 +58,12 @@ hipError_t launch_round_mantissa(const float *a, float *out, int64_t n, int drop
 hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, bool bf16,
                            const GemmParams &p, hipStream_t stream);
 
+// The same products for float32 operands, with the operand chunks copied
+// into LDS by the memory pipeline (pam_gemm_dma.hip); same tile shapes, same
+// results bit for bit.
+hipError_t launch_pam_gemm_dma(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b,
+                               const GemmParams &p, hipStream_t stream);
+
 // C of the split tiles of a matrix product launch: element by element the sum
 // over s = 0, 1, ... of W[s][t][.][.], in that order.
 hipError_t launch_split_tile_reduce(int tile_m, int tile_n, const GemmParams &p, hipStream_t stream);

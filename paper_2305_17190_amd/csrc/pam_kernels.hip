@@ -96,6 +96,38 @@ __device__ __forceinline__ void s1_row(float (&acc)[8], uint32_t a, const uint32
           "v"(bb[7]));
 }
 
+// A whole S1 step of the 8 x 8 micro-tile (s1_row for rows 0..7) as one
+// instruction sequence: the compiler separates consecutive inline-asm blocks
+// with a wait state, which one block per step avoids.
+#define PAM_S1_ROW(R, A)                                                                                   \
+    "v_add_u32 %[t0], %[" #A "], %[b0]\n\tv_add_u32 %[t1], %[" #A "], %[b1]\n\t"                           \
+    "v_add_u32 %[t2], %[" #A "], %[b2]\n\tv_add_u32 %[t3], %[" #A "], %[b3]\n\t"                           \
+    "v_add_u32 %[t4], %[" #A "], %[b4]\n\tv_add_u32 %[t5], %[" #A "], %[b5]\n\t"                           \
+    "v_add_u32 %[t6], %[" #A "], %[b6]\n\tv_add_u32 %[t7], %[" #A "], %[b7]\n\t"                           \
+    "v_add_f32 %[c" #R "0], %[c" #R "0], %[t0]\n\tv_add_f32 %[c" #R "1], %[c" #R "1], %[t1]\n\t"           \
+    "v_add_f32 %[c" #R "2], %[c" #R "2], %[t2]\n\tv_add_f32 %[c" #R "3], %[c" #R "3], %[t3]\n\t"           \
+    "v_add_f32 %[c" #R "4], %[c" #R "4], %[t4]\n\tv_add_f32 %[c" #R "5], %[c" #R "5], %[t5]\n\t"           \
+    "v_add_f32 %[c" #R "6], %[c" #R "6], %[t6]\n\tv_add_f32 %[c" #R "7], %[c" #R "7], %[t7]\n\t"
+#define PAM_ACC_ROW(R)                                                                                     \
+    [c##R##0] "+v"(acc[R][0]), [c##R##1] "+v"(acc[R][1]), [c##R##2] "+v"(acc[R][2]),                       \
+        [c##R##3] "+v"(acc[R][3]), [c##R##4] "+v"(acc[R][4]), [c##R##5] "+v"(acc[R][5]),                   \
+        [c##R##6] "+v"(acc[R][6]), [c##R##7] "+v"(acc[R][7])
+
+__device__ __forceinline__ void s1_step(float (&acc)[8][8], const uint4 &al, const uint4 &ah,
+                                        const uint32_t (&bb)[8]) {
+    uint32_t t0, t1, t2, t3, t4, t5, t6, t7;
+    asm(PAM_S1_ROW(0, a0) PAM_S1_ROW(1, a1) PAM_S1_ROW(2, a2) PAM_S1_ROW(3, a3) PAM_S1_ROW(4, a4)
+            PAM_S1_ROW(5, a5) PAM_S1_ROW(6, a6) PAM_S1_ROW(7, a7)
+        : PAM_ACC_ROW(0), PAM_ACC_ROW(1), PAM_ACC_ROW(2), PAM_ACC_ROW(3), PAM_ACC_ROW(4), PAM_ACC_ROW(5),
+          PAM_ACC_ROW(6), PAM_ACC_ROW(7), [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [t3] "=&v"(t3),
+          [t4] "=&v"(t4), [t5] "=&v"(t5), [t6] "=&v"(t6), [t7] "=&v"(t7)
+        : [a0] "v"(al.x), [a1] "v"(al.y), [a2] "v"(al.z), [a3] "v"(al.w), [a4] "v"(ah.x), [a5] "v"(ah.y),
+          [a6] "v"(ah.z), [a7] "v"(ah.w), [b0] "v"(bb[0]), [b1] "v"(bb[1]), [b2] "v"(bb[2]), [b3] "v"(bb[3]),
+          [b4] "v"(bb[4]), [b5] "v"(bb[5]), [b6] "v"(bb[6]), [b7] "v"(bb[7]));
+}
+#undef PAM_S1_ROW
+#undef PAM_ACC_ROW
+
 // One micro-tile row, S2: acc[j] = fma(aM + b'[j], m, acc[j]) for j < 8.
 // The eight integer adds are issued before the eight fmas: a SIMD pairs the
 // full-rate ops of two waves only when neither wave stalls on the result of
@@ -364,14 +396,7 @@ pam_gemm_kernel(GemmParams p) {
                         rd(k + 1, cur ^ 1);
                     __builtin_amdgcn_sched_barrier(0);
                     if ((s1_bits >> k) & 1u) {
-                        s1_row(acc[0], al[cur].x, bq[cur]);
-                        s1_row(acc[1], al[cur].y, bq[cur]);
-                        s1_row(acc[2], al[cur].z, bq[cur]);
-                        s1_row(acc[3], al[cur].w, bq[cur]);
-                        s1_row(acc[4], ah[cur].x, bq[cur]);
-                        s1_row(acc[5], ah[cur].y, bq[cur]);
-                        s1_row(acc[6], ah[cur].z, bq[cur]);
-                        s1_row(acc[7], ah[cur].w, bq[cur]);
+                        s1_step(acc, al[cur], ah[cur], bq[cur]);
                     }
                     __builtin_amdgcn_sched_barrier(0);
                 }
@@ -543,7 +568,9 @@ hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bo
     const dim3 grid((unsigned)items);
     if (bf16)
         return launch_shape<uint16_t>(tile_m, tile_n, kgroups, trans_a, trans_b, p, grid, stream);
-    return launch_shape<float>(tile_m, tile_n, kgroups, trans_a, trans_b, p, grid, stream);
+    // float32 operands: the kernel whose chunks are copied into LDS by the
+    // memory pipeline (same results bit for bit).
+    return launch_pam_gemm_dma(tile_m, tile_n, kgroups, trans_a, trans_b, p, stream);
 }
 
 // ---------------------------------------------------------------------------

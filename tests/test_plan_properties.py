@@ -1,8 +1,9 @@
 """Properties of the library's plan choice over random sizes (host logic, no
 GPU): a valid tile shape and split count, K slices of at least four chunks,
-hybrid plans whose whole-K tiles fill whole rounds of resident workgroups and
-split only the last one (or one and a half), and a workspace size that
-matches the plan."""
+hybrid plans (one k-group only) that split the tiles of a partial last round,
+of the last round and that one, or a quarter or half of a round's slots, into
+at least four slices (about one per 20 chunks, up to 16), and a workspace size
+that matches the plan."""
 import ctypes
 
 from hypothesis import given, settings, strategies as st
@@ -10,7 +11,7 @@ from hypothesis import given, settings, strategies as st
 import paper_2305_17190_amd as pam
 
 # Resident workgroups of each tile shape on the 256 compute units.
-SLOTS = {(128, 128, 1): 3 * 256, (128, 64, 1): 4 * 256, (128, 64, 2): 2 * 256, (64, 64, 1): 8 * 256,
+SLOTS = {(128, 128, 1): 4 * 256, (128, 64, 1): 6 * 256, (128, 64, 2): 3 * 256, (64, 64, 1): 8 * 256,
          (64, 64, 4): 2 * 256}
 
 
@@ -30,8 +31,9 @@ def test_plans_are_valid(m, n, k, batch):
         assert 0 <= whole < tiles
         if whole:
             slots = SLOTS[(tm, tn, kg)]
-            assert whole % slots == 0
-            assert tiles - whole in (tiles % slots, tiles % slots + slots)
+            assert kg == 1
+            assert tiles - whole in (tiles % slots, tiles % slots + slots, slots // 4, slots // 2)
+            assert splits >= max(4, min(16, -(-k // 16) // 20)) or -(-k // -(-k // splits)) < splits
     else:
         assert whole == 0
     size = ctypes.c_size_t()
@@ -45,16 +47,16 @@ def test_plans_are_valid(m, n, k, batch):
 
 
 # The plans the library picks for the benchmark products (tile_m, tile_n,
-# splits, k-groups, whole-K tiles), each measured within a few per cent of the
-# fastest plan of an exhaustive sweep: a change of the cost model that moves
-# one of them has to be measured again.
+# splits, k-groups, whole-K tiles), measured against the fastest plan of an
+# exhaustive sweep: within 0.4% on w2, w4 and w5, 1-8% on w3's products: a
+# change of the cost model that moves one of them has to be measured again.
 WORKLOAD_PLANS = {
-    (2, "fwd"): (128, 128, 1, 1, 0), (2, "dX"): (128, 64, 3, 1, 0), (2, "dW"): (128, 64, 53, 1, 0),
-    (3, "up"): (128, 128, 2, 1, 768), (3, "down"): (128, 128, 8, 1, 0), (3, "dH"): (128, 128, 2, 1, 768),
-    (3, "dW2"): (128, 128, 32, 1, 0), (3, "dX"): (128, 128, 8, 1, 0), (3, "dW1"): (128, 128, 32, 1, 0),
+    (2, "fwd"): (128, 64, 1, 2, 0), (2, "dX"): (128, 64, 4, 2, 0), (2, "dW"): (128, 64, 53, 1, 0),
+    (3, "up"): (128, 128, 1, 1, 0), (3, "down"): (128, 128, 4, 1, 0), (3, "dH"): (128, 128, 1, 1, 0),
+    (3, "dW2"): (128, 128, 16, 1, 0), (3, "dX"): (128, 128, 4, 1, 0), (3, "dW1"): (128, 128, 16, 1, 0),
     (4, "QKt"): (128, 128, 1, 1, 0), (4, "PV"): (128, 64, 1, 2, 0), (4, "dP"): (128, 128, 1, 1, 0),
     (4, "dV"): (128, 64, 1, 2, 0), (4, "dQ"): (128, 64, 1, 2, 0), (4, "dK"): (128, 64, 1, 2, 0),
-    (5, "fwd"): (128, 128, 8, 1, 3840), (5, "dX"): (128, 128, 8, 1, 3840), (5, "dW"): (128, 128, 8, 1, 768),
+    (5, "fwd"): (128, 128, 16, 1, 3840), (5, "dX"): (128, 128, 16, 1, 3840), (5, "dW"): (128, 128, 16, 1, 768),
 }
 
 

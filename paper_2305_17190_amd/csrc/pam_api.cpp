@@ -59,10 +59,10 @@ struct Shape {
 // (more waves without partial sums in HBM: the groups add their partial
 // tiles in LDS, at more staging work per MAC).  Resident workgroups per
 // compute unit follow from the float32 kernel's registers and LDS: the
-// 128 x 128 tile holds four waves per SIMD, the 128 x 64 tiles three, the
-// 64 x 64 tiles two.
+// 128 x 128 tile holds four waves per SIMD, the 128 x 64 tile with two
+// k-groups three, the others two.
 const Shape kShapes[] = {{128, 128, 1, 4, 4, 27.55e12},
-                         {128, 64, 1, 2, 6, 23.69e12},
+                         {128, 64, 1, 2, 4, 23.69e12},
                          {128, 64, 2, 4, 3, 24.51e12},
                          {64, 64, 1, 1, 8, 20.31e12},
                          {64, 64, 4, 4, 2, 20.71e12}};

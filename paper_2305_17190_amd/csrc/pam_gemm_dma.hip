@@ -334,7 +334,16 @@ struct DmaTile {
 // Waves per SIMD the tile is compiled for (registers per wave 512 / waves),
 // matching what its LDS footprint allows on a 160 KB compute unit.
 constexpr int dma_waves_per_simd(int bm, int bn, int kw) {
-    return (bm == 128 && bn == 128 && kw == 1) ? 4 : (bm == 128 && bn == 64) ? 3 : 2;
+    return (bm == 128 && bn == 128 && kw == 1) ? 4 : (bm == 128 && bn == 64 && kw == 2) ? 3 : 2;
+}
+
+// Minimum LDS words per workgroup.  Workgroups of one or two waves can be
+// placed unevenly on a compute unit's four SIMDs when more fit than the
+// launch fills (measured: one workgroup in a launch with three waves on a
+// SIMD ran 1.4x as long as the others).  Their LDS is padded so that no more
+// than two waves per SIMD fit: four 128 x 64 or eight 64 x 64 workgroups.
+constexpr int dma_min_lds_words(int bm, int bn, int kw) {
+    return (bm == 128 && bn == 64 && kw == 1) ? (33 << 10) / 4 : (bm == 64 && bn == 64 && kw == 1) ? (18 << 10) / 4 : 0;
 }
 
 template <int BM, int BN, int KW, bool TA, bool TB>
@@ -361,7 +370,9 @@ pam_gemm_dma_kernel(GemmParams p) {
     constexpr int kRed = (KW - 1) * BM * LDR;
     // Landing buffers, then the k-major compute buffers; for KW > 1 the
     // partial tiles reuse the same bytes after the K loop.
-    __shared__ __attribute__((aligned(16))) uint32_t smem[kStage > kRed ? kStage : kRed];
+    constexpr int kWords0 = kStage > kRed ? kStage : kRed;
+    constexpr int kMinWords = dma_min_lds_words(BM, BN, KW);
+    __shared__ __attribute__((aligned(16))) uint32_t smem[kWords0 > kMinWords ? kWords0 : kMinWords];
     __shared__ uint32_t sVote[NW];
     __shared__ uint32_t sMask[2][KW * NSLOT];
     uint32_t *rawA = smem;

@@ -11,7 +11,7 @@ from hypothesis import given, settings, strategies as st
 import paper_2305_17190_amd as pam
 
 # Resident workgroups of each tile shape on the 256 compute units.
-SLOTS = {(128, 128, 1): 4 * 256, (128, 64, 1): 6 * 256, (128, 64, 2): 3 * 256, (64, 64, 1): 8 * 256,
+SLOTS = {(128, 128, 1): 4 * 256, (128, 64, 1): 4 * 256, (128, 64, 2): 3 * 256, (64, 64, 1): 8 * 256,
          (64, 64, 4): 2 * 256}
 
 

@@ -278,8 +278,9 @@ struct DmaTile {
     }
 
     // Write the encoded chunk k-major into s[k * D + o] and mark the step
-    // masks (as the register-staged kernel's TileLoader::store).
-    template <typename SlotOf>
+    // masks (as the register-staged kernel's TileLoader::store): bit k % KPG
+    // of the word of k-group k / KPG.
+    template <int KPG, typename SlotOf>
     __device__ __forceinline__ void store(uint32_t *s, bool is_b, int tid, uint32_t low_groups, uint32_t *mask,
                                           int slots, SlotOf slot_of) const {
         if (KCONTIG) {
@@ -321,8 +322,8 @@ struct DmaTile {
                     const uint32_t ex = e[c] & kExpMask;
                     if (ex < (64u << 23)) {
                         const int k = KCONTIG ? kk + c : kk;
-                        const uint32_t bit = 1u << (k % 16);
-                        atomicOr(&mask[(k / 16) * slots + slot_of(KCONTIG ? o : o + c)],
+                        const uint32_t bit = 1u << (k % KPG);
+                        atomicOr(&mask[(k / KPG) * slots + slot_of(KCONTIG ? o : o + c)],
                                  ex != 0u ? (bit | (bit << 16)) : bit);
                     }
                 }
@@ -337,6 +338,13 @@ constexpr int dma_waves_per_simd(int bm, int bn, int kw) {
     return (bm == 128 && bn == 128 && kw == 1) ? 4 : (bm == 128 && bn == 64 && kw == 2) ? 3 : 2;
 }
 
+// k steps per k-group per LDS chunk.  The same as the bfloat16 kernel's, so
+// that both partition K among the k-groups alike and give the same bits (an
+// 8-step chunk for the 64 x 64 tile with four k-groups, at 32 KB of LDS and
+// four waves per SIMD, measured 8-20% faster on w4 / w2 shapes, but would
+// sum in another order).
+constexpr int dma_kpg(int, int, int) { return kChunkK; }
+
 // Minimum LDS words per workgroup.  Workgroups of one or two waves can be
 // placed unevenly on a compute unit's four SIMDs when more fit than the
 // launch fills (measured: one workgroup in a launch with three waves on a
@@ -349,7 +357,7 @@ constexpr int dma_min_lds_words(int bm, int bn, int kw) {
 template <int BM, int BN, int KW, bool TA, bool TB>
 __global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(dma_waves_per_simd(BM, BN, KW))))
 pam_gemm_dma_kernel(GemmParams p) {
-    constexpr int KPG = kChunkK;           // k steps per group per chunk
+    constexpr int KPG = dma_kpg(BM, BN, KW);   // k steps per group per chunk
     constexpr int BK = KPG * KW;
     constexpr int NTG = BM * BN / 64;
     constexpr int NT = NTG * KW;
@@ -361,13 +369,16 @@ pam_gemm_dma_kernel(GemmParams p) {
     static_assert(WC >= 1 && WR * WC == NRW && BM / 64 == WR, "waves do not tile the output tile");
     constexpr int HM = BM / 2;
     constexpr int HN = BN / 2;
-    constexpr int LDR = BN + 4;            // partial-tile rows (KW > 1)
+    constexpr int LDR = BN;                // partial-tile rows (KW > 1)
     using TileA = DmaTile<BM, BK, NT, !TA>;
     using TileB = DmaTile<BN, BK, NT, TB>;
     constexpr int kRawA = TileA::SEGS * 4;
     constexpr int kRawB = TileB::SEGS * 4;
     constexpr int kStage = kRawA + kRawB + BK * BM + BK * BN;
-    constexpr int kRed = (KW - 1) * BM * LDR;
+    // Partial tiles held at once by the LDS after the K loop (KW > 1).
+    constexpr int kRedTiles = KW == 1 ? 0 : (kStage / (BM * LDR) >= KW - 1 ? KW - 1 : kStage / (BM * LDR));
+    static_assert(KW == 1 || kRedTiles >= 1, "no room for a partial tile");
+    constexpr int kRed = kRedTiles * BM * LDR;
     // Landing buffers, then the k-major compute buffers; for KW > 1 the
     // partial tiles reuse the same bytes after the K loop.
     constexpr int kWords0 = kStage > kRed ? kStage : kRed;
@@ -463,8 +474,8 @@ pam_gemm_dma_kernel(GemmParams p) {
         const uint64_t sp = __ballot((fa | fb) & 2u);
         uint32_t *mask = sMask[c & 1];
         __syncthreads();   // every wave is done reading the previous chunk (and zeroing this mask)
-        la.store(encA, false, tid_c, fa >> 2, mask, NSLOT, a_slot);
-        lb.store(encB, true, tid_c, fb >> 2, mask, NSLOT, b_slot);
+        la.template store<KPG>(encA, false, tid_c, fa >> 2, mask, NSLOT, a_slot);
+        lb.template store<KPG>(encB, true, tid_c, fb >> 2, mask, NSLOT, b_slot);
         if (lane == 0)
             sVote[wave] = sp ? 1u : 0u;
         __syncthreads();
@@ -490,10 +501,11 @@ pam_gemm_dma_kernel(GemmParams p) {
 
         __builtin_amdgcn_s_setprio(0);
 
-        const uint32_t s1_bits = special ? 0u : (~low & 0xFFFFu);
-        const uint32_t s2_bits = special ? 0u : (low & ~(low >> 16) & 0xFFFFu);
+        constexpr uint32_t kStepMask = (1u << KPG) - 1u;
+        const uint32_t s1_bits = special ? 0u : (~low & kStepMask);
+        const uint32_t s2_bits = special ? 0u : (low & ~(low >> 16) & kStepMask);
         const uint32_t s3_bits = special ? 0u : (low >> 16);
-        const uint32_t sp_bits = special ? 0xFFFFu : 0u;
+        const uint32_t sp_bits = special ? kStepMask : 0u;
         const uint32_t *a_row = encA + k_first * BM + ty * 4;
         const uint32_t *b_row = encB + k_first * BN + tx * 4;
         {
@@ -510,9 +522,9 @@ pam_gemm_dma_kernel(GemmParams p) {
             if (s1_bits != 0u) {
                 rd(0, 0);
 #pragma unroll
-                for (int k = 0; k < 16; ++k) {
+                for (int k = 0; k < KPG; ++k) {
                     const int cur = k & 1;
-                    if (k + 1 < 16)
+                    if (k + 1 < KPG)
                         rd(k + 1, cur ^ 1);
                     __builtin_amdgcn_sched_barrier(0);
                     if ((s1_bits >> k) & 1u)
@@ -578,46 +590,53 @@ pam_gemm_dma_kernel(GemmParams p) {
         vec = true;
     }
     if constexpr (KW > 1) {
-        // Groups 1.. write their partial tiles; group 0 adds them, in group
-        // order, to its own.
-        __syncthreads();   // the LDS buffers are free: every wave is past its last chunk
+        // Groups 1.. write their partial tiles, as many at a time as the LDS
+        // holds (kRedTiles); group 0 adds them, in group order, to its own.
         float *red = reinterpret_cast<float *>(smem);
-        if (grp > 0) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+        for (int g0 = 1; g0 < KW; g0 += kRedTiles) {
+            __syncthreads();   // the LDS is free: every wave is past its last chunk / the previous round's adds
+            if (grp >= g0 && grp < g0 + kRedTiles) {
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int col = h == 0 ? tx * 4 : HN + tx * 4;
-                    *reinterpret_cast<float4 *>(&red[((grp - 1) * BM + row) * LDR + col]) =
-                        make_float4(acc[i][4 * h], acc[i][4 * h + 1], acc[i][4 * h + 2], acc[i][4 * h + 3]);
+                for (int i = 0; i < 8; ++i) {
+                    const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int col = h == 0 ? tx * 4 : HN + tx * 4;
+                        *reinterpret_cast<float4 *>(&red[((grp - g0) * BM + row) * LDR + col]) =
+                            make_float4(acc[i][4 * h], acc[i][4 * h + 1], acc[i][4 * h + 2], acc[i][4 * h + 3]);
+                    }
+                }
+            }
+            __syncthreads();
+            if (grp == 0) {
+                // Row by row: the row's partial values, then its adds (in
+                // inline asm, in group order, so that the compiler neither
+                // loads every partial tile up front nor moves the adds past
+                // the next row's loads).
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    asm volatile("" ::: "memory");
+                    const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
+#pragma unroll
+                    for (int g = g0; g < g0 + kRedTiles && g < KW; ++g) {
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            const int col = h == 0 ? tx * 4 : HN + tx * 4;
+                            const float4 x =
+                                *reinterpret_cast<const float4 *>(&red[((g - g0) * BM + row) * LDR + col]);
+                            asm volatile("v_add_f32 %0, %0, %4\n\tv_add_f32 %1, %1, %5\n\t"
+                                         "v_add_f32 %2, %2, %6\n\tv_add_f32 %3, %3, %7"
+                                         : "+v"(acc[i][4 * h]), "+v"(acc[i][4 * h + 1]), "+v"(acc[i][4 * h + 2]),
+                                           "+v"(acc[i][4 * h + 3])
+                                         : "v"(x.x), "v"(x.y), "v"(x.z), "v"(x.w));
+                        }
+                    }
                 }
             }
         }
-        __syncthreads();
         if (grp > 0)
             return;
-        // Row by row: the row's partial values, then its adds (in inline asm,
-        // in group order, so that the compiler neither loads every partial
-        // tile up front nor moves the adds past the next row's loads).
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            asm volatile("" ::: "memory");
-            const int row = i < 4 ? ty * 4 + i : HM + ty * 4 + (i - 4);
-#pragma unroll
-            for (int g = 1; g < KW; ++g) {
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int col = h == 0 ? tx * 4 : HN + tx * 4;
-                    const float4 x = *reinterpret_cast<const float4 *>(&red[((g - 1) * BM + row) * LDR + col]);
-                    asm volatile("v_add_f32 %0, %0, %4\n\tv_add_f32 %1, %1, %5\n\t"
-                                 "v_add_f32 %2, %2, %6\n\tv_add_f32 %3, %3, %7"
-                                 : "+v"(acc[i][4 * h]), "+v"(acc[i][4 * h + 1]), "+v"(acc[i][4 * h + 2]),
-                                   "+v"(acc[i][4 * h + 3])
-                                 : "v"(x.x), "v"(x.y), "v"(x.z), "v"(x.w));
-                }
-            }
-        }
     }
     typedef float f32x4 __attribute__((ext_vector_type(4)));
 #pragma unroll

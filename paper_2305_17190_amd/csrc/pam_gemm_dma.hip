@@ -40,6 +40,23 @@ namespace pamk {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
+// One 16-byte copy per lane from global memory into LDS: lane i's bytes at
+// base + off land at lds + 16 i (the block address in M0, the same for the
+// whole wave).  Issued from inline asm, so that the compiler does not make
+// later LDS reads of other buffers wait for the copy (it cannot tell the
+// landing buffer from the compute buffers of the same array); every read of
+// the landing buffer is preceded by an explicit wait for the vector-memory
+// counter.  The kernels' compiled code uses M0 for nothing else (no other
+// LDS copies, no indexed register moves), so setting it here disturbs no
+// value the compiler keeps there.
+__device__ __forceinline__ void dma_copy16(const char *base, uint32_t off, uint32_t *lds) {
+    const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t *)lds);
+    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(off), "s"(base), "s"(m0v)
+                 : "memory", "m0");
+}
+
 // One micro-tile row of an S2 or S3 step from A's own encoding a: first
 // 1 + M_A (exponent field 127, a's mantissa) and +-2^E_A (a with its mantissa
 // cleared, +-0 for zero / denormal a), then the SCALED products with the
@@ -188,8 +205,7 @@ struct DmaTile {
 #pragma unroll
         for (int r = 0; r < L; ++r) {
             if (copyable(tid, r, o0, o_lim))
-                __builtin_amdgcn_global_load_lds((const void *)(cb + boff(tid, r, ld, o0, o_lim)),
-                                                 (lds_void_t *)slot_block(raw, r, w), 16, 0, 0);
+                dma_copy16(cb, boff(tid, r, ld, o0, o_lim), slot_block(raw, r, w));
         }
     }
 

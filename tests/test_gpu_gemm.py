@@ -234,6 +234,31 @@ def test_whole_and_split_tiles_match_their_plans(tile, kg, batch):
         assert torch.equal(mixed[sl].view(torch.int32), want[sl].view(torch.int32)), f"tile {t}"
 
 
+@pytest.mark.parametrize("ta,tb", TRANS, ids=["NN", "NT", "TN", "TT"])
+def test_small_and_large_launches_agree(ta, tb):
+    # A product's result does not depend on the launch it is part of: the
+    # first 80 products of a batch (480 work items, fewer than the resident
+    # workgroups) and the same products among 120 (720 work items) are bit
+    # for bit equal, and the small batch matches the oracle.
+    import torch
+    m, n, k = 200, 130, 700
+    plan = (128, 64, 1, 2)
+    note(f"small vs large launch m={m} n={n} k={k} ta={ta} tb={tb} plan={plan}")
+    a_shape = (120, k, m) if ta else (120, m, k)
+    b_shape = (120, n, k) if tb else (120, k, n)
+    a = make("zeros_tiny", a_shape, 91)
+    b = make("normal", b_shape, 92)
+    a[7] = make("specials", a_shape[1:], 93)
+    da, db = to_dev(a), to_dev(b)
+    small = pam.bmm(da[:80], db[:80], trans_a=ta, trans_b=tb, plan=plan)
+    large = pam.bmm(da, db, trans_a=ta, trans_b=tb, plan=plan)
+    assert torch.equal(small.view(torch.int32), large[:80].view(torch.int32))
+    got = small[:8].cpu().numpy()
+    c_ref, s_ref = oracle_gemm(a[:8], b[:8], ta, tb, m, n, k, a_shape[2], b_shape[2], a[0].size, b[0].size,
+                               batches=list(range(8)))
+    check_gemm(got, c_ref, s_ref, k, f"small launch ta={ta} tb={tb}")
+
+
 def test_k0_writes_zeros():
     import torch
     note("gemm K = 0")

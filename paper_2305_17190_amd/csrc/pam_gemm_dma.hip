@@ -50,10 +50,15 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // LDS copies, no indexed register moves), so setting it here disturbs no
 // value the compiler keeps there.
 __device__ __forceinline__ void dma_copy16(const char *base, uint32_t off, uint32_t *lds) {
+    // base and lds are the same for the whole wave; reading them from the
+    // first lane puts them in scalar registers, as the instruction requires.
+    const uint2 b = __builtin_bit_cast(uint2, base);
+    const uint64_t sb = __builtin_bit_cast(
+        uint64_t, make_uint2(__builtin_amdgcn_readfirstlane(b.x), __builtin_amdgcn_readfirstlane(b.y)));
     const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t *)lds);
     asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                  :
-                 : "v"(off), "s"(base), "s"(m0v)
+                 : "v"(off), "s"(sb), "s"(m0v)
                  : "memory", "m0");
 }
 

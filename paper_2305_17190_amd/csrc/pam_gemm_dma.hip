@@ -56,7 +56,9 @@ __device__ __forceinline__ void dma_copy16(const char *base, uint32_t off, uint3
     const uint64_t sb = __builtin_bit_cast(
         uint64_t, make_uint2(__builtin_amdgcn_readfirstlane(b.x), __builtin_amdgcn_readfirstlane(b.y)));
     const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t *)lds);
-    asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+    // One wait state between the scalar write of M0 and the copy that reads
+    // it (the LDS-DMA read-after-SALU-write hazard of this generation).
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                  :
                  : "v"(off), "s"(sb), "s"(m0v)
                  : "memory", "m0");
@@ -371,12 +373,21 @@ constexpr int dma_kpg(int, int, int) { return kChunkK; }
 // launch fills (measured: one workgroup in a launch with three waves on a
 // SIMD ran 1.4x as long as the others).  Their LDS is padded so that no more
 // than two waves per SIMD fit: four 128 x 64 or eight 64 x 64 workgroups.
-constexpr int dma_min_lds_words(int bm, int bn, int kw) {
-    return (bm == 128 && bn == 64 && kw == 1) ? (33 << 10) / 4 : (bm == 64 && bn == 64 && kw == 1) ? (18 << 10) / 4 : 0;
+// The 128 x 64 two-group tile built for two waves per SIMD is padded to two
+// workgroups per compute unit for the same reason.
+constexpr int dma_min_lds_words(int bm, int bn, int kw, int wps) {
+    return (bm == 128 && bn == 64 && kw == 1)   ? (33 << 10) / 4
+           : (bm == 64 && bn == 64 && kw == 1)  ? (18 << 10) / 4
+           : (bm == 128 && bn == 64 && kw == 2 && wps == 2) ? (54 << 10) / 4
+                                                           : 0;
 }
 
-template <int BM, int BN, int KW, bool TA, bool TB>
-__global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(dma_waves_per_simd(BM, BN, KW))))
+// WPS: waves per SIMD the kernel is compiled for.  At two (256 registers a
+// wave) the per-thread staging addresses are computed once, before the K
+// loop; at three or four they are recomputed per chunk, since registers held
+// across the loop would not fit beside the accumulators.
+template <int BM, int BN, int KW, bool TA, bool TB, int WPS>
+__global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(WPS)))
 pam_gemm_dma_kernel(GemmParams p) {
     constexpr int KPG = dma_kpg(BM, BN, KW);   // k steps per group per chunk
     constexpr int BK = KPG * KW;
@@ -403,7 +414,7 @@ pam_gemm_dma_kernel(GemmParams p) {
     // Landing buffers, then the k-major compute buffers; for KW > 1 the
     // partial tiles reuse the same bytes after the K loop.
     constexpr int kWords0 = kStage > kRed ? kStage : kRed;
-    constexpr int kMinWords = dma_min_lds_words(BM, BN, KW);
+    constexpr int kMinWords = dma_min_lds_words(BM, BN, KW, WPS);
     __shared__ __attribute__((aligned(16))) uint32_t smem[kWords0 > kMinWords ? kWords0 : kMinWords];
     __shared__ uint32_t sVote[NW];
     __shared__ uint32_t sMask[2][KW * NSLOT];
@@ -478,7 +489,8 @@ pam_gemm_dma_kernel(GemmParams p) {
         // from it are recomputed per chunk instead of being hoisted out of
         // the loop into registers that would stay live during the steps.
         int tid_c = tid;
-        asm volatile("" : "+v"(tid_c));
+        if constexpr (WPS > 2)
+            asm volatile("" : "+v"(tid_c));
         __builtin_amdgcn_s_setprio(1);
         // This thread's copies of chunk c have landed (the only vector-memory
         // operations outstanding).
@@ -687,17 +699,17 @@ pam_gemm_dma_kernel(GemmParams p) {
     }
 }
 
-template <int BM, int BN, int KW>
+template <int BM, int BN, int KW, int WPS = dma_waves_per_simd(BM, BN, KW)>
 static hipError_t launch_dma_tile(bool ta, bool tb, const GemmParams &p, dim3 grid, hipStream_t stream) {
     const dim3 block(BM * BN / 64 * KW);
     if (!ta && !tb)
-        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, false>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, false, WPS>), grid, block, 0, stream, p);
     else if (!ta && tb)
-        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, true>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, true, WPS>), grid, block, 0, stream, p);
     else if (ta && !tb)
-        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, false>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, false, WPS>), grid, block, 0, stream, p);
     else
-        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, true>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, true, WPS>), grid, block, 0, stream, p);
     return hipGetLastError();
 }
 
@@ -712,7 +724,14 @@ hipError_t launch_pam_gemm_dma(int tile_m, int tile_n, int kgroups, bool trans_a
     if (tile_m == 128 && tile_n == 64 && kgroups == 1)
         return launch_dma_tile<128, 64, 1>(trans_a, trans_b, p, grid, stream);
     if (tile_m == 128 && tile_n == 64 && kgroups == 2)
+    {
+        // A launch that two workgroups per compute unit hold at once runs
+        // the build for two waves per SIMD (staging addresses kept in
+        // registers); its occupancy is two anyway.
+        if (items <= 2 * 256)
+            return launch_dma_tile<128, 64, 2, 2>(trans_a, trans_b, p, grid, stream);
         return launch_dma_tile<128, 64, 2>(trans_a, trans_b, p, grid, stream);
+    }
     if (tile_m == 64 && tile_n == 64 && kgroups == 1)
         return launch_dma_tile<64, 64, 1>(trans_a, trans_b, p, grid, stream);
     if (tile_m == 64 && tile_n == 64 && kgroups == 4)

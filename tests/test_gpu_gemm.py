@@ -238,8 +238,11 @@ def test_whole_and_split_tiles_match_their_plans(tile, kg, batch):
 def test_small_and_large_launches_agree(ta, tb):
     # A product's result does not depend on the launch it is part of: the
     # first 80 products of a batch (480 work items, fewer than the resident
-    # workgroups) and the same products among 120 (720 work items) are bit
-    # for bit equal, and the small batch matches the oracle.
+    # workgroups; the kernel built for two waves per SIMD) and the same
+    # products among 120 (720 work items; built for three) are bit for bit
+    # equal, NaN payloads aside (the two builds may add the operands of a
+    # SPECIAL step's sum in either order, and a sum of two NaNs keeps one of
+    # them), and the small batch matches the oracle.
     import torch
     m, n, k = 200, 130, 700
     plan = (128, 64, 1, 2)
@@ -252,7 +255,10 @@ def test_small_and_large_launches_agree(ta, tb):
     da, db = to_dev(a), to_dev(b)
     small = pam.bmm(da[:80], db[:80], trans_a=ta, trans_b=tb, plan=plan)
     large = pam.bmm(da, db, trans_a=ta, trans_b=tb, plan=plan)
-    assert torch.equal(small.view(torch.int32), large[:80].view(torch.int32))
+    same_nan = torch.isnan(small) == torch.isnan(large[:80])
+    assert bool(same_nan.all())
+    fin = ~torch.isnan(small)
+    assert torch.equal(small[fin].view(torch.int32), large[:80][fin].view(torch.int32))
     got = small[:8].cpu().numpy()
     c_ref, s_ref = oracle_gemm(a[:8], b[:8], ta, tb, m, n, k, a_shape[2], b_shape[2], a[0].size, b[0].size,
                                batches=list(range(8)))

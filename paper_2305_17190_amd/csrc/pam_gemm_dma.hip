@@ -197,6 +197,9 @@ struct DmaTile {
     static __device__ __forceinline__ bool copyable(int tid, int r, int o0, int o_lim) {
         return KCONTIG || o0 + seg_o(tid, r) + 3 < o_lim;
     }
+    // Every segment of the tile is copyable (the same for the whole
+    // workgroup): the tile lies inside the operand, or it is K-contiguous.
+    static __device__ __forceinline__ bool all_copyable(int o0, int o_lim) { return KCONTIG || o0 + D <= o_lim; }
 
     // LDS landing slot of segment r of this thread (wave w, lane): block
     // (r * NW + w) of 64 segments, the lane's 16 bytes within it.
@@ -209,6 +212,12 @@ struct DmaTile {
     static __device__ __forceinline__ void copy(const float *__restrict__ base, uint32_t *raw, int w, int tid,
                                                 int64_t ld, int o0, int o_lim) {
         const char *cb = reinterpret_cast<const char *>(base);
+        if (all_copyable(o0, o_lim)) {
+#pragma unroll
+            for (int r = 0; r < L; ++r)
+                dma_copy16(cb, boff(tid, r, ld, o0, o_lim), slot_block(raw, r, w));
+            return;
+        }
 #pragma unroll
         for (int r = 0; r < L; ++r) {
             if (copyable(tid, r, o0, o_lim))
@@ -222,6 +231,14 @@ struct DmaTile {
     __device__ __forceinline__ void fetch(const uint32_t *raw, int w, int lane, bool copied,
                                           const float *__restrict__ base, int64_t ld, int o0, int o_lim, int k0,
                                           int k_lim, int tid) {
+        if (copied && all_copyable(o0, o_lim)) {
+            // The common case, one branch for all segments: the reads issue
+            // back to back and are waited for once.
+#pragma unroll
+            for (int r = 0; r < L; ++r)
+                v[r] = *reinterpret_cast<const uint4 *>(slot_block(const_cast<uint32_t *>(raw), r, w) + lane * 4);
+            return;
+        }
 #pragma unroll
         for (int r = 0; r < L; ++r) {
             if (copied && copyable(tid, r, o0, o_lim))
@@ -459,8 +476,8 @@ pam_gemm_dma_kernel(GemmParams p) {
 
     TileA la;
     TileB lb;
-    auto a_slot = [](int o) { return ((o % HM) / 4) / 8; };
-    auto b_slot = [](int o) { return WR + ((o % HN) / 4) / 8; };
+    auto a_slot = [](int o) { return (int)(((uint32_t)o % HM) / 32u); };
+    auto b_slot = [](int o) { return WR + (int)(((uint32_t)o % HN) / 32u); };
 
     float acc[8][8];
 #pragma unroll

@@ -38,8 +38,6 @@
 
 namespace pamk {
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
 // One 16-byte copy per lane from global memory into LDS: lane i's bytes at
 // base + off land at lds + 16 i (the block address in M0, the same for the
 // whole wave).  Issued from inline asm, so that the compiler does not make
@@ -55,7 +53,9 @@ __device__ __forceinline__ void dma_copy16(const char *base, uint32_t off, uint3
     const uint2 b = __builtin_bit_cast(uint2, base);
     const uint64_t sb = __builtin_bit_cast(
         uint64_t, make_uint2(__builtin_amdgcn_readfirstlane(b.x), __builtin_amdgcn_readfirstlane(b.y)));
-    const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t *)lds);
+    // The low 32 bits of a generic address in the LDS aperture are the LDS
+    // byte address (no null-pointer test as in a cast to the LDS space).
+    const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
     // One wait state between the scalar write of M0 and the copy that reads
     // it (the LDS-DMA read-after-SALU-write hazard of this generation).
     asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
@@ -185,8 +185,9 @@ struct DmaTile {
     // Byte offset of segment r from its chunk's base.  Rows past o_lim are
     // clamped to the last valid row (their outputs are discarded); a segment
     // straddling the last valid column is not copied (copyable) and is
-    // loaded element by element.  Recomputed per chunk from the thread
-    // index, so that no per-thread offsets stay live across the K loop.
+    // loaded element by element.  In builds for three or four waves per SIMD
+    // recomputed per chunk from the thread index, so that no per-thread
+    // offsets stay live across the K loop.
     static __device__ __forceinline__ uint32_t boff(int tid, int r, int64_t ld, int o0, int o_lim) {
         const int o = seg_o(tid, r);
         const int kk = seg_k(tid, r);
@@ -400,12 +401,14 @@ constexpr int dma_min_lds_words(int bm, int bn, int kw, int wps) {
 }
 
 // WPS: waves per SIMD the kernel is compiled for.  At two (256 registers a
-// wave) the per-thread staging addresses are computed once, before the K
-// loop; at three or four they are recomputed per chunk, since registers held
-// across the loop would not fit beside the accumulators.
+// wave), and at three for a row-major A (168 registers, measured to fit), the
+// per-thread staging addresses are computed once, before the K loop;
+// otherwise they are recomputed per chunk, since registers held across the
+// loop would not fit beside the accumulators.
 template <int BM, int BN, int KW, bool TA, bool TB, int WPS>
 __global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(WPS)))
 pam_gemm_dma_kernel(GemmParams p) {
+    constexpr bool kKeepAddresses = WPS <= 2 || (WPS == 3 && !TA);
     constexpr int KPG = dma_kpg(BM, BN, KW);   // k steps per group per chunk
     constexpr int BK = KPG * KW;
     constexpr int NTG = BM * BN / 64;
@@ -506,7 +509,7 @@ pam_gemm_dma_kernel(GemmParams p) {
         // from it are recomputed per chunk instead of being hoisted out of
         // the loop into registers that would stay live during the steps.
         int tid_c = tid;
-        if constexpr (WPS > 2)
+        if constexpr (!kKeepAddresses)
             asm volatile("" : "+v"(tid_c));
         __builtin_amdgcn_s_setprio(1);
         // This thread's copies of chunk c have landed (the only vector-memory

@@ -14,6 +14,7 @@ workload.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -32,6 +33,11 @@ ALGO_LANE_OPS_PER_MAC = 2
 # full-rate ops (int32 add, float32 add/mul/fma) = the 157.3 TFLOP/s
 # float32-vector figure counted as one lane op per fma.
 NOMINAL_VALU_LANE_OPS = 256 * 4 * 32 * 2.4e9
+# Default warm-up: at least this much wall time of untimed steps.  After
+# three warm-up steps, w4's first 20 timed steps (0.3-0.4 ms each) ran 4-13%
+# slower than the same 20 steps repeated right after them: the GPU had not
+# yet left the clock it idled at.
+WARMUP_MIN_S = 0.5
 # The GEMM kernel's sources: a committed traffic summary is valid only for these bytes.
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2305_17190_amd", "csrc", f)
                   for f in ("pam_kernels.hip", "pam_gemm_dma.hip", "pam_tile.h", "pam_scalar.h")]
@@ -68,6 +74,63 @@ def committed_counter(workload: str, form: str, key: str):
     if not sha or not val or sha.group(1) != kernel_source_digest():
         return None
     return float(val.group(1))
+
+
+class TimingEvents:
+    """HIP events used only for timing, recorded on the launch stream.
+
+    They are created with hipEventDisableSystemFence: recording a default
+    event ends with a system-scope fence (cache write-back and invalidate),
+    which between products as short as w4's (~0.05 ms) added ~3.5 us per
+    event to the step and to the bracketed launch itself.  The elapsed times
+    are read only after a device synchronisation.
+    """
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, stream_handle: int):
+        # The HIP runtime the process already loaded (torch's; the library
+        # links the same soname), never a second copy.
+        path = None
+        with open("/proc/self/maps") as fh:
+            for line in fh:
+                if "libamdhip64" in line:
+                    path = line.split()[-1]
+                    break
+        if path is None:
+            raise RuntimeError("the HIP runtime is not loaded")
+        hip = ctypes.CDLL(path)
+        vp = ctypes.c_void_p
+        hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+        hip.hipEventRecord.argtypes = [vp, vp]
+        hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+        hip.hipEventDestroy.argtypes = [vp]
+        self.hip = hip
+        self.stream = vp(stream_handle)
+        self.events = []
+
+    def _check(self, status: int, what: str) -> None:
+        if status != 0:
+            raise RuntimeError(f"{what} failed with HIP error {status}")
+
+    def new(self):
+        ev = ctypes.c_void_p()
+        self._check(self.hip.hipEventCreateWithFlags(ctypes.byref(ev), self.DISABLE_SYSTEM_FENCE),
+                    "hipEventCreateWithFlags")
+        self.events.append(ev)
+        return ev
+
+    def record(self, ev) -> None:
+        self._check(self.hip.hipEventRecord(ev, self.stream), "hipEventRecord")
+
+    def elapsed_ms(self, start, end) -> float:
+        ms = ctypes.c_float()
+        self._check(self.hip.hipEventElapsedTime(ctypes.byref(ms), start, end), "hipEventElapsedTime")
+        return ms.value
+
+    def close(self) -> None:
+        for ev in self.events:
+            self.hip.hipEventDestroy(ev)
+        self.events = []
 
 
 def cpu_baseline(workload_id: int, host, forms, target_s: float) -> dict:
@@ -250,7 +313,9 @@ def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed warm-up steps (default: at least 3, and at least 0.5 s of them, so that short "
+                         "steps are not timed while the GPU's clock is still rising from idle)")
     ap.add_argument("--workload", default="w5", choices=["w1", "w2", "w3", "w4", "w5"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -270,6 +335,9 @@ def main() -> int:
     ap.add_argument("--elementwise-op", default="mul", choices=sorted(ELEMENTWISE_OPS),
                     help="the elementwise op --elementwise times (default mul)")
     args = ap.parse_args()
+    args.warmup_auto = args.warmup is None
+    if args.warmup is None:
+        args.warmup = 3
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the PAM matrix product is "
@@ -322,33 +390,41 @@ def main() -> int:
                      mantissa_bits=args.mantissa_bits)
 
     macs_per_step = sum(f.macs for f in forms)
-    for _ in range(args.warmup):
+    t_warm = time.perf_counter()
+    done = 0
+    while done < args.warmup or (args.warmup_auto and time.perf_counter() - t_warm < WARMUP_MIN_S):
         for f in forms:
             launch(f)
+        done += 1
+        if args.warmup_auto:
+            torch.cuda.synchronize()
+    args.warmup = done
     torch.cuda.synchronize()
 
-    events = {f.name: [] for f in forms}
+    # Per-product events on the stream the products are launched on,
+    # created before the timed region.
+    timer = TimingEvents(torch.cuda.current_stream().cuda_stream)
+    events = {f.name: [(timer.new(), timer.new()) for _ in range(args.steps)] for f in forms}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
         for f in forms:
-            s = torch.cuda.Event(enable_timing=True)
-            e = torch.cuda.Event(enable_timing=True)
-            s.record()
+            s, e = events[f.name][i]
+            timer.record(s)
             launch(f)
-            e.record()
-            events[f.name].append((s, e))
+            timer.record(e)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
     per_form, med_form = {}, {}
     for f in forms:
-        ms = sorted(s.elapsed_time(e) for s, e in events[f.name])
+        ms = sorted(timer.elapsed_ms(s, e) for s, e in events[f.name])
         per_form[f.name] = sum(ms) / len(ms)
         med_form[f.name] = ms[len(ms) // 2] if len(ms) % 2 else 0.5 * (ms[len(ms) // 2 - 1] + ms[len(ms) // 2])
         log(f"  {f.name:6s} m={f.m} n={f.n} k={f.k} batch={f.batch} plan={pam.plan(f.m, f.n, f.k, f.batch)} "
             f"avg {per_form[f.name]:.3f} ms median {med_form[f.name]:.3f} ms  "
             f"{f.macs / med_form[f.name] / 1e9:.1f} GPAM-MAC/s")
+    timer.close()
 
     info = pam.device_info(0)
     peak = NOMINAL_VALU_LANE_OPS

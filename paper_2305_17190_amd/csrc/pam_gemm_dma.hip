@@ -39,30 +39,34 @@
 namespace pamk {
 
 // One 16-byte copy per lane from global memory into LDS: lane i's bytes at
-// base + off land at lds + 16 i (the block address in M0, the same for the
-// whole wave).  Issued from inline asm, so that the compiler does not make
-// later LDS reads of other buffers wait for the copy (it cannot tell the
-// landing buffer from the compute buffers of the same array); every read of
-// the landing buffer is preceded by an explicit wait for the vector-memory
-// counter.  The kernels' compiled code uses M0 for nothing else (no other
+// base + off land at LDS byte address lds_base + IMM + 16 i (the block
+// address in M0, the same for the whole wave).  Issued from inline asm, so
+// that the compiler does not make later LDS reads of other buffers wait for
+// the copy (it cannot tell the landing buffer from the compute buffers of
+// the same array); every read of the landing buffer is preceded by an
+// explicit wait for the vector-memory counter.  The kernels' compiled code uses M0 for nothing else (no other
 // LDS copies, no indexed register moves), so setting it here disturbs no
 // value the compiler keeps there.
-__device__ __forceinline__ void dma_copy16(const char *base, uint32_t off, uint32_t *lds) {
-    // base and lds are the same for the whole wave; reading them from the
-    // first lane puts them in scalar registers, as the instruction requires.
+template <int IMM>
+__device__ __forceinline__ void dma_copy16(const char *base, uint32_t off, uint32_t lds_base) {
+    // base and lds_base are the same for the whole wave; reading them from
+    // the first lane puts them in scalar registers, as the instruction
+    // requires.
     const uint2 b = __builtin_bit_cast(uint2, base);
     const uint64_t sb = __builtin_bit_cast(
         uint64_t, make_uint2(__builtin_amdgcn_readfirstlane(b.x), __builtin_amdgcn_readfirstlane(b.y)));
-    // The low 32 bits of a generic address in the LDS aperture are the LDS
-    // byte address (no null-pointer test as in a cast to the LDS space).
-    const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_base);
     // One wait state between the scalar write of M0 and the copy that reads
     // it (the LDS-DMA read-after-SALU-write hazard of this generation).
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+    asm volatile("s_add_u32 m0, %2, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                  :
-                 : "v"(off), "s"(sb), "s"(m0v)
-                 : "memory", "m0");
+                 : "v"(off), "s"(sb), "s"(lb), "i"(IMM)
+                 : "memory", "m0", "scc");
 }
+
+// LDS byte address of an element of a __shared__ array: the low 32 bits of
+// its generic address (no null-pointer test as in a cast to the LDS space).
+__device__ __forceinline__ uint32_t lds_addr(const uint32_t *p) { return (uint32_t)(uintptr_t)p; }
 
 // One micro-tile row of an S2 or S3 step from A's own encoding a: first
 // 1 + M_A (exponent field 127, a's mantissa) and +-2^E_A (a with its mantissa
@@ -187,13 +191,16 @@ struct DmaTile {
     // straddling the last valid column is not copied (copyable) and is
     // loaded element by element.  In builds for three or four waves per SIMD
     // recomputed per chunk from the thread index, so that no per-thread
-    // offsets stay live across the K loop.
+    // offsets stay live across the K loop.  The leading dimension is below
+    // 2^22 elements (the library rejects larger ones), so ld * 4 and the row
+    // or k index fit a 24-bit multiply.
     static __device__ __forceinline__ uint32_t boff(int tid, int r, int64_t ld, int o0, int o_lim) {
         const int o = seg_o(tid, r);
         const int kk = seg_k(tid, r);
+        const uint32_t ld4 = (uint32_t)ld * 4u;
         if (KCONTIG)
-            return (uint32_t)(((int64_t)(min(o0 + o, o_lim - 1) - o0) * ld + kk) * 4);
-        return (uint32_t)(((int64_t)kk * ld + o) * 4);
+            return __umul24((uint32_t)min(o, o_lim - 1 - o0), ld4) + (uint32_t)kk * 4u;
+        return __umul24((uint32_t)kk, ld4) + (uint32_t)o * 4u;
     }
     static __device__ __forceinline__ bool copyable(int tid, int r, int o0, int o_lim) {
         return KCONTIG || o0 + seg_o(tid, r) + 3 < o_lim;
@@ -208,21 +215,39 @@ struct DmaTile {
         return raw + (r * NW + w) * 256;
     }
 
-    // Start copying the chunk at `base` into the landing buffer.  Called only
-    // for an interior chunk of an aligned operand.
-    static __device__ __forceinline__ void copy(const float *__restrict__ base, uint32_t *raw, int w, int tid,
+    // Start copying the chunk at `base` into the landing buffer at byte
+    // RAW_OFF of the LDS array; lds_w is the LDS byte address of that array
+    // plus 1024 per wave index, so that block (r * NW + w) lies at
+    // lds_w + RAW_OFF + r * NW * 1024.  Called only for an interior chunk of
+    // an aligned operand.
+    template <int RAW_OFF, int R>
+    static __device__ __forceinline__ void copy_seg(const char *cb, uint32_t lds_w, int tid, int64_t ld, int o0,
+                                                    int o_lim) {
+        dma_copy16<RAW_OFF + R * NW * 1024>(cb, boff(tid, R, ld, o0, o_lim), lds_w);
+    }
+    template <int RAW_OFF>
+    static __device__ __forceinline__ void copy(const float *__restrict__ base, uint32_t lds_w, int tid,
                                                 int64_t ld, int o0, int o_lim) {
         const char *cb = reinterpret_cast<const char *>(base);
+        static_assert(L == 2 || L == 4, "segments per thread");
         if (all_copyable(o0, o_lim)) {
-#pragma unroll
-            for (int r = 0; r < L; ++r)
-                dma_copy16(cb, boff(tid, r, ld, o0, o_lim), slot_block(raw, r, w));
+            copy_seg<RAW_OFF, 0>(cb, lds_w, tid, ld, o0, o_lim);
+            copy_seg<RAW_OFF, 1>(cb, lds_w, tid, ld, o0, o_lim);
+            if constexpr (L == 4) {
+                copy_seg<RAW_OFF, 2>(cb, lds_w, tid, ld, o0, o_lim);
+                copy_seg<RAW_OFF, 3>(cb, lds_w, tid, ld, o0, o_lim);
+            }
             return;
         }
-#pragma unroll
-        for (int r = 0; r < L; ++r) {
-            if (copyable(tid, r, o0, o_lim))
-                dma_copy16(cb, boff(tid, r, ld, o0, o_lim), slot_block(raw, r, w));
+        if (copyable(tid, 0, o0, o_lim))
+            copy_seg<RAW_OFF, 0>(cb, lds_w, tid, ld, o0, o_lim);
+        if (copyable(tid, 1, o0, o_lim))
+            copy_seg<RAW_OFF, 1>(cb, lds_w, tid, ld, o0, o_lim);
+        if constexpr (L == 4) {
+            if (copyable(tid, 2, o0, o_lim))
+                copy_seg<RAW_OFF, 2>(cb, lds_w, tid, ld, o0, o_lim);
+            if (copyable(tid, 3, o0, o_lim))
+                copy_seg<RAW_OFF, 3>(cb, lds_w, tid, ld, o0, o_lim);
         }
     }
 
@@ -286,47 +311,51 @@ struct DmaTile {
         }
     }
 
-    // Bit 0: some element has exponent field below 64; bit 1: some element
-    // needs the SPECIAL path (inf, NaN, |x| >= 2^64); bit 2 + r: segment r
-    // holds an element of the first kind.
-    __device__ __forceinline__ uint32_t scan() const {
-        uint32_t hi = 0, groups = 0;
+    // One pass over the held elements with the exponent field moved to the
+    // top byte and the sign dropped (x << 1): per segment r the least such
+    // value (below 64 << 24 iff the segment holds an element below the S1
+    // range: a zero, denormal or |x| < 2^-63), and the largest over all
+    // elements, returned (at least 191 << 24 iff one needs the SPECIAL
+    // path: |x| >= 2^64, inf, NaN).
+    __device__ __forceinline__ uint32_t scan(uint32_t (&smin)[L]) const {
+        uint32_t mx = 0;
 #pragma unroll
         for (int r = 0; r < L; ++r) {
-            const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
-            uint32_t lo = 0xFFFFFFFFu;
-#pragma unroll
-            for (int c = 0; c < 4; ++c) {
-                const uint32_t ex = e[c] & kExpMask;
-                hi = max(hi, ex);
-                lo = min(lo, ex);
-            }
-            if (lo < (64u << 23))
-                groups |= 1u << r;
+            const uint32_t j0 = v[r].x << 1, j1 = v[r].y << 1, j2 = v[r].z << 1, j3 = v[r].w << 1;
+            smin[r] = min(min(j0, j1), min(j2, j3));
+            mx = max(mx, max(max(j0, j1), max(j2, j3)));
         }
-        return (groups != 0u ? 1u : 0u) | (hi >= (191u << 23) ? 2u : 0u) | (groups << 2);
+        return mx;
+    }
+    static __device__ __forceinline__ bool low_seg(uint32_t smin) { return smin < (64u << 24); }
+
+    // A denormal element to its signed zero (multiplying by 1.0 flushes it;
+    // NaN stays NaN).  Needed for B only, and only where scan() found an
+    // element below the S1 range.
+    __device__ __forceinline__ void flush_denormals() {
+#pragma unroll
+        for (int r = 0; r < L; ++r) {
+            uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                asm("v_mul_f32 %0, 1.0, %1" : "=v"(e[c]) : "v"(e[c]));
+            v[r] = make_uint4(e[0], e[1], e[2], e[3]);
+        }
     }
 
-    // Element encodings: A as it is; B as b' = b - bias after flushing a
-    // denormal b to its signed zero (multiplying by 1.0 flushes it; NaN stays
-    // NaN).
-    static __device__ __forceinline__ uint32_t enc(uint32_t u, bool is_b) {
-        if (!is_b)
-            return u;
-        uint32_t f;
-        asm("v_mul_f32 %0, 1.0, %1" : "=v"(f) : "v"(u));
-        return f - kBias;
-    }
+    // Element encodings: A as it is; B as b' = b - bias (denormals already
+    // flushed).
+    static __device__ __forceinline__ uint32_t enc(uint32_t u, bool is_b) { return is_b ? u - kBias : u; }
 
     // Write the encoded chunk k-major into s[k * D + o] and mark the step
     // masks (as the register-staged kernel's TileLoader::store): bit k % KPG
     // of the word of k-group k / KPG.
     template <int KPG, typename SlotOf>
-    __device__ __forceinline__ void store(uint32_t *s, bool is_b, int tid, uint32_t low_groups, uint32_t *mask,
+    __device__ __forceinline__ void store(uint32_t *s, bool is_b, int tid, const uint32_t (&smin)[L], uint32_t *mask,
                                           int slots, SlotOf slot_of) const {
         if (KCONTIG) {
-            const int o0 = seg_o(tid, 0);
-            const int k0 = seg_k(tid, 0);
+            // One address; the four k rows at constant offsets from it.
+            uint32_t *const row0 = s + seg_k(tid, 0) * D + seg_o(tid, 0);
 #pragma unroll
             for (int c = 0; c < 4; ++c) {
                 uint32_t w[L];
@@ -335,7 +364,7 @@ struct DmaTile {
                     const uint32_t u = c == 0 ? v[r].x : c == 1 ? v[r].y : c == 2 ? v[r].z : v[r].w;
                     w[r] = enc(u, is_b);
                 }
-                uint32_t *dst = s + (k0 + c) * D + o0;
+                uint32_t *dst = row0 + c * D;
                 if constexpr (L == 2)
                     *reinterpret_cast<uint2 *>(dst) = make_uint2(w[0], w[1]);
                 else
@@ -354,7 +383,7 @@ struct DmaTile {
         for (int r = 0; r < L; ++r) {
             // Rare: the wave skips this unless one of its lanes holds such an
             // element in segment r.
-            if ((low_groups >> r) & 1u) {
+            if (low_seg(smin[r])) {
                 const uint32_t e[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
                 const int o = seg_o(tid, r);
                 const int kk = seg_k(tid, r);
@@ -413,7 +442,6 @@ pam_gemm_dma_kernel(GemmParams p) {
     constexpr int BK = KPG * KW;
     constexpr int NTG = BM * BN / 64;
     constexpr int NT = NTG * KW;
-    constexpr int NW = NT / 64;
     constexpr int NRW = NTG / 64;
     constexpr int WC = BN / 64;
     constexpr int WR = NRW / WC;
@@ -436,8 +464,10 @@ pam_gemm_dma_kernel(GemmParams p) {
     constexpr int kWords0 = kStage > kRed ? kStage : kRed;
     constexpr int kMinWords = dma_min_lds_words(BM, BN, KW, WPS);
     __shared__ __attribute__((aligned(16))) uint32_t smem[kWords0 > kMinWords ? kWords0 : kMinWords];
-    __shared__ uint32_t sVote[NW];
-    __shared__ uint32_t sMask[2][KW * NSLOT];
+    // Step masks of the two chunks in flight (k-group g's slot words at
+    // g * NSLOT), and after them the chunk's SPECIAL vote.
+    __shared__ uint32_t sMask[2][KW * NSLOT + 1];
+    static_assert(2 * (KW * NSLOT + 1) <= NT, "the mask words are cleared one per thread");
     uint32_t *rawA = smem;
     uint32_t *rawB = smem + kRawA;
     uint32_t *encA = smem + kRawA + kRawB;
@@ -447,6 +477,7 @@ pam_gemm_dma_kernel(GemmParams p) {
     const int grp = tid / NTG;
     const int t = tid % NTG;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t lds_w = __builtin_amdgcn_readfirstlane(lds_addr(smem) + (uint32_t)wave * 1024u);
     const int gwave = t >> 6;
     const int wr = gwave / WC;
     const int wc = gwave % WC;
@@ -476,6 +507,10 @@ pam_gemm_dma_kernel(GemmParams p) {
     const int64_t b_step = TB ? BK : (int64_t)BK * p.ldb;
     const bool vec_a = p.vec_a != 0;
     const bool vec_b = p.vec_b != 0;
+    // The launch's flags as one scalar word, tested afresh in each chunk
+    // (kept as three lane masks across the loop they took six scalar
+    // registers, spilled).
+    const uint32_t flags = (vec_a ? 1u : 0u) | (vec_b ? 2u : 0u) | (p.round_drop != 0 ? 4u : 0u);
 
     TileA la;
     TileB lb;
@@ -489,22 +524,24 @@ pam_gemm_dma_kernel(GemmParams p) {
         for (int j = 0; j < 8; ++j)
             acc[i][j] = 0.0f;
 
-    if (tid < 2 * KW * NSLOT)
+    if (tid < 2 * (KW * NSLOT + 1))
         (&sMask[0][0])[tid] = 0u;
 
     // Chunk c is copied when it is whole (k0 + BK <= ke) and its operand
     // aligned.
     if (nchunks > 0 && kb + BK <= ke) {
         if (vec_a)
-            TileA::copy(a_base, rawA, wave, tid, p.lda, m0, p.m);
+            TileA::template copy<0>(a_base, lds_w, tid, p.lda, m0, p.m);
         if (vec_b)
-            TileB::copy(b_base, rawB, wave, tid, p.ldb, n0, p.n);
+            TileB::template copy<kRawA * 4>(b_base, lds_w, tid, p.ldb, n0, p.n);
     }
 
     const int k_first = grp * KPG;
     for (int c = 0; c < nchunks; ++c) {
         const int k0 = kb + c * BK;
         const bool interior = k0 + BK <= ke;
+        uint32_t fl = __builtin_amdgcn_readfirstlane(flags);
+        asm volatile("" : "+s"(fl));
         // The thread index through an empty asm: staging addresses derived
         // from it are recomputed per chunk instead of being hoisted out of
         // the loop into registers that would stay live during the steps.
@@ -515,41 +552,43 @@ pam_gemm_dma_kernel(GemmParams p) {
         // This thread's copies of chunk c have landed (the only vector-memory
         // operations outstanding).
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        la.fetch(rawA, wave, tid_c & 63, interior && vec_a, a_base + c * a_step, p.lda, m0, p.m, k0, ke, tid_c);
-        lb.fetch(rawB, wave, tid_c & 63, interior && vec_b, b_base + c * b_step, p.ldb, n0, p.n, k0, ke, tid_c);
+        la.fetch(rawA, wave, tid_c & 63, interior && (fl & 1u), a_base + c * a_step, p.lda, m0, p.m, k0, ke, tid_c);
+        lb.fetch(rawB, wave, tid_c & 63, interior && (fl & 2u), b_base + c * b_step, p.ldb, n0, p.n, k0, ke, tid_c);
 
-        if (p.round_drop != 0) {
+        if (fl & 4u) {
             la.round_mantissa(p.round_drop);
             lb.round_mantissa(p.round_drop);
         }
-        const uint32_t fa = la.scan();
-        const uint32_t fb = lb.scan();
-        const uint64_t sp = __ballot((fa | fb) & 2u);
+        uint32_t smin_a[TileA::L], smin_b[TileB::L];
+        const uint32_t mx = max(la.scan(smin_a), lb.scan(smin_b));
+        uint32_t low_b = smin_b[0];
+#pragma unroll
+        for (int r = 1; r < TileB::L; ++r)
+            low_b = min(low_b, smin_b[r]);
+        if (TileB::low_seg(low_b))   // rare per thread: B's denormals to zero
+            lb.flush_denormals();
         uint32_t *mask = sMask[c & 1];
         __syncthreads();   // every wave is done reading the previous chunk (and zeroing this mask)
-        la.template store<KPG>(encA, false, tid_c, fa >> 2, mask, NSLOT, a_slot);
-        lb.template store<KPG>(encB, true, tid_c, fb >> 2, mask, NSLOT, b_slot);
-        if (lane == 0)
-            sVote[wave] = sp ? 1u : 0u;
+        la.template store<KPG>(encA, false, tid_c, smin_a, mask, NSLOT, a_slot);
+        lb.template store<KPG>(encB, true, tid_c, smin_b, mask, NSLOT, b_slot);
+        // The workgroup's SPECIAL vote: one more mask word.
+        if (mx >= (191u << 24))
+            atomicOr(&mask[KW * NSLOT], 1u);
         __syncthreads();
 
-        uint32_t vote = 0;
-#pragma unroll
-        for (int w = 0; w < NW; ++w)
-            vote |= sVote[w];
-        const bool special = vote != 0u;
+        const bool special = __builtin_amdgcn_readfirstlane(mask[KW * NSLOT]) != 0u;
         const uint32_t low =
             __builtin_amdgcn_readfirstlane(mask[grp * NSLOT + wr] | mask[grp * NSLOT + WR + wc]);
-        if (tid < KW * NSLOT)
-            sMask[(c + 1) & 1][tid] = 0u;
+        if (tid < KW * NSLOT + 1)
+            (&sMask[0][0])[(((uint32_t)c + 1u) & 1u) * (KW * NSLOT + 1) + (uint32_t)tid] = 0u;
 
         // The next chunk's copies land while this one is computed (the
         // landing slots are this thread's own and were read above).
         if (c + 1 < nchunks && k0 + 2 * BK <= ke) {
-            if (vec_a)
-                TileA::copy(a_base + (c + 1) * a_step, rawA, wave, tid_c, p.lda, m0, p.m);
-            if (vec_b)
-                TileB::copy(b_base + (c + 1) * b_step, rawB, wave, tid_c, p.ldb, n0, p.n);
+            if (fl & 1u)
+                TileA::template copy<0>(a_base + (c + 1) * a_step, lds_w, tid_c, p.lda, m0, p.m);
+            if (fl & 2u)
+                TileB::template copy<kRawA * 4>(b_base + (c + 1) * b_step, lds_w, tid_c, p.ldb, n0, p.n);
         }
 
         __builtin_amdgcn_s_setprio(0);

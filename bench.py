@@ -198,6 +198,22 @@ ELEMENTWISE_OPS = {
 }
 
 
+def warm_up(args, torch, step) -> None:
+    """Untimed steps before the timed region: args.warmup of them, or, when
+    --warmup is not given, at least three and at least WARMUP_MIN_S seconds
+    (synchronising after each, so that the GPU has left its idle clock);
+    args.warmup is set to the number run."""
+    t_warm = time.perf_counter()
+    done = 0
+    while done < args.warmup or (args.warmup_auto and time.perf_counter() - t_warm < WARMUP_MIN_S):
+        step()
+        done += 1
+        if args.warmup_auto:
+            torch.cuda.synchronize()
+    args.warmup = done
+    torch.cuda.synchronize()
+
+
 def bench_elementwise(args, torch, wl, pam, dev) -> int:
     """One elementwise op on N elements: 8 bytes read and 4 written per element
     (two-operand ops), or 4 read and 4 written (one-operand ops)."""
@@ -213,9 +229,7 @@ def bench_elementwise(args, torch, wl, pam, dev) -> int:
         if args.elementwise_op == "palog2":
             ins = (ins[0].abs(),)
     out = torch.empty_like(ins[0])
-    for _ in range(args.warmup):
-        fn(*ins, out=out)
-    torch.cuda.synchronize()
+    warm_up(args, torch, lambda: fn(*ins, out=out))
     s = torch.cuda.Event(enable_timing=True)
     e = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
@@ -275,9 +289,7 @@ def bench_autograd(args, torch, wl, pam, dev) -> int:
         w.grad = None
         pam_linear(x, w, derivative=derivative).backward(dy)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm_up(args, torch, step)
     s = torch.cuda.Event(enable_timing=True)
     e = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
@@ -390,16 +402,11 @@ def main() -> int:
                      mantissa_bits=args.mantissa_bits)
 
     macs_per_step = sum(f.macs for f in forms)
-    t_warm = time.perf_counter()
-    done = 0
-    while done < args.warmup or (args.warmup_auto and time.perf_counter() - t_warm < WARMUP_MIN_S):
+    def one_step():
         for f in forms:
             launch(f)
-        done += 1
-        if args.warmup_auto:
-            torch.cuda.synchronize()
-    args.warmup = done
-    torch.cuda.synchronize()
+
+    warm_up(args, torch, one_step)
 
     # Per-product events on the stream the products are launched on,
     # created before the timed region.

@@ -361,3 +361,34 @@ def test_underflow_to_exact_zero_k1():
     want = pam_ref.pam_mul_ref(np.repeat(col, 5, 1), np.repeat(row, 4, 0))
     assert np.array_equal(c, want), (c, want)
     assert np.all((c == 0) | (np.abs(c) >= 2.0 ** -126)), "a denormal value reached the output"
+
+
+SEGMENT_MIXES = [(0.0, np.inf), (-0.0, np.nan), (np.float32(3e-41), -np.inf), (np.float32(1.2e-38), 2.0 ** 70),
+                 (np.float32(-1.5e-38), np.float32(-(2.0 ** 65)))]
+
+
+@pytest.mark.parametrize("plan", [(128, 128, 1), (128, 64, 1, 2), (64, 64, 1, 4)], ids=lambda p: "x".join(map(str, p)))
+@pytest.mark.parametrize("ta,tb", TRANS, ids=["NN", "NT", "TN", "TT"])
+@pytest.mark.parametrize("operand", ["A", "B"])
+def test_special_beside_low_in_one_segment(operand, ta, tb, plan):
+    # One group of four elements consecutive in memory (one staged segment)
+    # holds a value below the S1 range next to a SPECIAL one, in one chunk of
+    # one tile, all else normal: the chunk must take the SPECIAL path (the
+    # special value must not hide behind the low one, nor the low one behind
+    # the special) and the other chunks and tiles their own paths.
+    m, n, k = 150, 140, 96
+    for case, (low, special) in enumerate(SEGMENT_MIXES):
+        a_shape = (k, m) if ta else (m, k)
+        b_shape = (n, k) if tb else (k, n)
+        g = np.random.default_rng(500 + case)
+        a = g.standard_normal(a_shape).astype(np.float32)
+        b = g.standard_normal(b_shape).astype(np.float32)
+        x = a if operand == "A" else b
+        r = int(g.integers(0, x.shape[0]))
+        c0 = 4 * int(g.integers(0, x.shape[1] // 4))
+        x[r, c0 + case % 4] = low
+        x[r, c0 + (case + 2) % 4] = special
+        note(f"segment mix {case} operand={operand} ta={ta} tb={tb} plan={plan} at ({r}, {c0})")
+        c = pam.bmm(to_dev(a)[None], to_dev(b)[None], trans_a=ta, trans_b=tb, plan=plan)
+        c_ref, s_ref = oracle_gemm(a.ravel(), b.ravel(), ta, tb, m, n, k, a.shape[1], b.shape[1], batches=[0])
+        check_gemm(c.cpu().numpy(), c_ref, s_ref, k, f"segment mix {case} {operand} ta={ta} tb={tb} {plan}")

@@ -48,8 +48,9 @@ def test_plans_are_valid(m, n, k, batch):
 
 # The plans the library picks for the benchmark products (tile_m, tile_n,
 # splits, k-groups, whole-K tiles), measured against the fastest plan of an
-# exhaustive sweep: within 0.4% on w2, w4 and w5, 1-8% on w3's products: a
-# change of the cost model that moves one of them has to be measured again.
+# exhaustive sweep: the best or within 0.3% on w2 and w4, within 0.9% on w5,
+# 1-4% behind on w3's products: a change of the cost model that moves one of
+# them has to be measured again.
 WORKLOAD_PLANS = {
     (2, "fwd"): (128, 64, 1, 2, 0), (2, "dX"): (128, 64, 4, 2, 0), (2, "dW"): (128, 64, 53, 1, 0),
     (3, "up"): (128, 128, 1, 1, 0), (3, "down"): (128, 128, 4, 1, 0), (3, "dH"): (128, 128, 1, 1, 0),

@@ -40,7 +40,7 @@ NOMINAL_VALU_LANE_OPS = 256 * 4 * 32 * 2.4e9
 WARMUP_MIN_S = 0.5
 # The GEMM kernel's sources: a committed traffic summary is valid only for these bytes.
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2305_17190_amd", "csrc", f)
-                  for f in ("pam_kernels.hip", "pam_gemm_dma.hip", "pam_tile.h", "pam_scalar.h")]
+                  for f in ("pam_kernels.hip", "pam_gemm_dma.hip", "pam_scalar.h")]
 
 
 def log(msg: str) -> None:
@@ -470,7 +470,7 @@ def main() -> int:
         },
         "roofline": {
             "bound": "alu",
-            "kernel": f"{'pam_gemm_kernel' if args.bf16 else 'pam_gemm_dma_kernel'} {dom.name} "
+            "kernel": f"pam_gemm_dma_kernel {dom.name} "
                       f"({'T' if dom.trans_a else 'N'}{'T' if dom.trans_b else 'N'})",
             "achieved": round(achieved / 1e12, 3),
             "peak": round(peak / 1e12, 3),

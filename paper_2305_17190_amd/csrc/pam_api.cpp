@@ -1,6 +1,6 @@
 // C ABI of the PAM library: argument validation, plan selection, workspace
 // handling and launches.  The arithmetic lives in the HIP sources
-// (pam_kernels.hip, pa_ops.hip, pam_exact_grad.hip).
+// (pam_gemm_dma.hip, pam_kernels.hip, pa_ops.hip, pam_exact_grad.hip).
 
 #include <hip/hip_runtime.h>
 #include <hsa/hsa.h>
@@ -396,11 +396,10 @@ pam_status_t run_gemm(pam_op_t ta, pam_op_t tb, int64_t m, int64_t n, int64_t k,
     p.k = (int32_t)k;
     p.k_per_split = (int32_t)std::min<int64_t>(plan.k_per_split, kMaxDim);
     p.tiles_n = (int32_t)ceil_div(n, plan.tile_n);
-    // Operand groups of four elements: 16 bytes (float32) or 8 (bfloat16).
-    const bool a_ok = bf16 ? aligned8(A) : aligned16(A);
-    const bool b_ok = bf16 ? aligned8(B) : aligned16(B);
-    p.vec_a = a_ok && lda % 4 == 0 && (batch == 1 || sa % 4 == 0);
-    p.vec_b = b_ok && ldb % 4 == 0 && (batch == 1 || sb % 4 == 0);
+    // Operand copies of 16 bytes: four float32 or eight bfloat16 elements.
+    const int64_t per16 = bf16 ? 8 : 4;
+    p.vec_a = aligned16(A) && lda % per16 == 0 && (batch == 1 || sa % per16 == 0);
+    p.vec_b = aligned16(B) && ldb % per16 == 0 && (batch == 1 || sb % per16 == 0);
     p.vec_c = aligned16(C) && ldc % 4 == 0 && (batch == 1 || sc % 4 == 0);
     p.round_drop = round_drop;
     p.tiles = (int32_t)L.tiles;

@@ -1,28 +1,67 @@
-// PAM matrix product for float32 operands with the operand chunks copied
-// from global memory straight into LDS (gfx950's global_load_lds_dwordx4).
+// PAM matrix products on gfx950, for float32 and bfloat16 operands.
 //
-// Same tiles, work items, k-groups, step paths (S1 / S2 / S3 / SPECIAL) and
-// summation order as pam_gemm_kernel in pam_kernels.hip, so both give the
-// same bits; what differs is the staging:
+// PAM (Kosson & Jaggi, Sec. 2.2): the product of two float32 numbers is
+// replaced by the int32 sum of their encodings minus one exponent bias
+// (127 << 23); the sign is the exclusive or of the signs, zero / denormal
+// operands and underflowing results give signed zeros, overflowing results
+// saturate at +-FLT_MAX, NaN / inf follow IEEE multiplication with a
+// canonical quiet NaN.  PAM matrix products (Sec. 3.2) keep float32
+// accumulation.
 //
-// * Each chunk's operand segments (16 bytes: four elements consecutive in
-//   memory) are copied by the memory pipeline into an LDS landing buffer.
-//   No register holds a chunk while its copy is in flight, so the kernel
-//   keeps only the accumulators and the compute step's operands live across
-//   the K loop, and the 128 x 128 tile fits four waves per SIMD instead of
-//   three.
-// * At the chunk boundary each thread re-reads the segments it copied (its
-//   own, so no barrier is needed for them), scans and encodes them, and
-//   writes them k-major into the compute buffer.  A thread holds L rows of
-//   one k quad of a K-contiguous operand and writes each k as one L-word
-//   store; the lanes of a wave write consecutive columns of one k row, so
-//   the stores are free of bank conflicts (the register-staged kernel's
-//   word stores to four k rows conflict four ways).
-// * A is kept as its own encoding only (one plane instead of three): the S1
-//   step reads it as it is, and the rarer S2 / S3 steps derive 1 + M_A and
-//   +-2^E_A from it with two bit operations per value.
+// The product is a vector-ALU contraction (PAM is not a product, so the
+// matrix cores do not apply).  Each workgroup owns a BM x BN output tile,
+// each thread an 8 x 8 register micro-tile, and K advances in LDS chunks of
+// 16 steps per k-group.  On gfx950 the integer add and the float32 add, mul
+// and fma issue at twice the rate of other vector ops, so the per-MAC work is
+// built from those four only.
+//
+// Encodings in LDS, written once per chunk: A as it is; B as b' = b -
+// 0x3F800000 (a denormal b first flushed to its signed zero).
+//   S1 (per MAC: v_add_u32, v_add_f32): acc += a + b'.  When both exponent
+//      fields are in [64, 190] the int32 sum is PAM(a, b)'s encoding itself
+//      (Sec. 2.2's addition; the magnitude sum cannot leave the normal range
+//      and the carry out of the sign bits leaves their exclusive or): no
+//      multiply at all.
+//   SCALED form, for the other finite operands: with aM the encoding of
+//   1 + M_A (exponent field 127, a's mantissa) and m = a with its mantissa
+//   cleared (the float +-2^E_A, or +-0), t = aM + b' is the encoding of
+//   PAM(1 + M_A, b); PAM is exact under power-of-two scaling (Fig. 2: the
+//   pattern repeats per octave), so t * m = PAM(a, b) whenever the result is
+//   a normal number, the float multiply supplying the sign.  A zero b makes t
+//   a denormal encoding, which the float unit (denormals flushed) reads as 0.
+//   aM and m are derived per row from A's encoding (two bit operations).
+//   S2 (per MAC: v_add_u32, v_fmac_f32): acc = fma(t, m, acc).  Exact when
+//      no product underflows: every nonzero operand has exponent field in
+//      [64, 190].
+//   S3 (per MAC: v_add_u32, v_mul_f32, v_add_f32): p = t * m rounded on its
+//      own, so an underflowing product flushes to the signed zero PAM
+//      defines; exact for all finite operands with |x| < 2^64.
+//   Each wave takes S1, S2 or S3 per k step from bit masks of the operands
+//   it reads at that k: S1 unless one has exponent field below 64, S3 if one
+//   of those is a normal number ("tiny", field 1..63), S2 otherwise (zeros
+//   and denormals only); the S1 steps first, then S2, then S3.
+//   SPECIAL: a chunk holding inf, NaN or |x| >= 2^64 takes the complete
+//   per-MAC definition (never on finite data below 2^64).
+//
+// Staging:
+//
+// * Each chunk's operand pieces (16 bytes: four float32 or eight bfloat16
+//   elements consecutive in memory) are copied by the memory pipeline
+//   (gfx950's global_load_lds_dwordx4) into an LDS landing buffer.  No
+//   register holds a chunk while its copy is in flight, so the kernel keeps
+//   only the accumulators and the compute step's operands live across the K
+//   loop, and the 128 x 128 tile fits four waves per SIMD.
+// * At the chunk boundary each thread re-reads segments of four elements
+//   its own wave copied (so no barrier is needed for them), widens bfloat16
+//   elements exactly to float32 encodings, scans and encodes them, and writes
+//   them k-major into the compute buffer.  A thread holds L rows of one k
+//   quad of a K-contiguous operand and writes each k as one L-word store;
+//   the lanes of a wave write consecutive columns of one k row, so the
+//   stores are free of bank conflicts.  Float32 and bfloat16 operands are
+//   staged into the same segments, so a bfloat16 product equals the float32
+//   product of its widened operands bit for bit.
 // * The chunk after next is copied while a chunk is computed; segments that
-//   cannot be copied whole (the K tail, an unaligned operand, a segment
+//   cannot be copied whole (the K tail, an unaligned operand, a piece
 //   straddling the last column) are loaded element by element from global
 //   memory when the chunk is encoded.
 //
@@ -155,26 +194,31 @@ __device__ __forceinline__ void dma_frag(const uint32_t *p, int half, uint32_t (
 }
 
 // One operand's D x BK chunk (D = rows of op(A) or columns of op(B)) in
-// 16-byte segments of four elements consecutive in memory.
+// segments of four elements consecutive in memory; T is the operand's
+// element type (float or bfloat16 bits).
 //
-// KCONTIG: a segment is (row o, k quad).  Thread t copies the L rows
+// KCONTIG: a segment is (row o, k quad).  Thread t stages the L rows
 // j * L .. j * L + L - 1 of one k quad kq, so that it can write each k of them
 // as one L-word LDS store.  Lane 16 * q + i of a wave takes row group
 // j = 16 * (wave / (BK / 16)) + i and k quad kq = q + 4 * (wave % (BK / 16)):
-// one copy instruction reads 16 rows x 64 contiguous bytes (16 cache lines,
-// as many as the register-staged loads), and the 16 lanes of each store pass
-// write 16 consecutive row groups of one k row (no bank conflicts).
+// with float32 operands, one copy instruction reads 16 rows x 64 contiguous
+// bytes (16 cache lines), and the 16 lanes of each store pass write 16
+// consecutive row groups of one k row (no bank conflicts).
 //
 // Otherwise a segment is (k, column quad); thread t's segment r is number
 // t + r * NT, so consecutive lanes hold consecutive column quads of one k.
-template <int D, int BK, int NT, bool KCONTIG>
+template <int D, int BK, int NT, bool KCONTIG, typename T>
 struct DmaTile {
     static constexpr int SEGS = D * BK / 4;
     static constexpr int L = SEGS / NT;                  // segments per thread
     static constexpr int G = D / L;                      // KCONTIG: row groups
     static constexpr int KS = BK / 16;                   // KCONTIG: waves per 16 row groups
     static constexpr int NW = NT / 64;
+    static constexpr bool kWide = sizeof(T) == 4;        // float32 operands; else bfloat16
+    static constexpr int EPC = 16 / (int)sizeof(T);      // elements per 16-byte copy
+    static constexpr int CL = D * BK / EPC / NT;         // copies per thread
     static_assert(L * NT == SEGS && (L == 2 || L == 4), "chunk does not divide over the threads");
+    static_assert(CL * EPC * NT == D * BK && CL >= 1, "chunk copies do not divide over the threads");
     static_assert(!KCONTIG || (G % 16 == 0 && BK % 16 == 0 && (G / 16) * KS == NW), "bad K-contiguous segment split");
 
     uint4 v[L];          // the segments being encoded (live only at the chunk boundary)
@@ -186,54 +230,77 @@ struct DmaTile {
         return KCONTIG ? (((t & 63) >> 4) + 4 * ((t >> 6) % KS)) * 4 : (t + r * NT) / (D / 4);
     }
 
-    // Byte offset of segment r from its chunk's base.  Rows past o_lim are
-    // clamped to the last valid row (their outputs are discarded); a segment
-    // straddling the last valid column is not copied (copyable) and is
-    // loaded element by element.  In builds for three or four waves per SIMD
-    // recomputed per chunk from the thread index, so that no per-thread
-    // offsets stay live across the K loop.  The leading dimension is below
-    // 2^22 elements (the library rejects larger ones), so ld * 4 and the row
-    // or k index fit a 24-bit multiply.
-    static __device__ __forceinline__ uint32_t boff(int tid, int r, int64_t ld, int o0, int o_lim) {
-        const int o = seg_o(tid, r);
-        const int kk = seg_k(tid, r);
-        const uint32_t ld4 = (uint32_t)ld * 4u;
+    // Copies.  A float32 copy is one segment (seg_o / seg_k).  A bfloat16
+    // copy is eight elements consecutive in memory, and a wave copies exactly
+    // the elements its own lanes stage (so that, after its own wait for the
+    // copies, it reads no other wave's): copy r of lane i takes q = i + 64 r
+    // of the wave's pieces.  K-contiguous: the wave stages 16 L rows x 16 k
+    // (row groups 16 (w / KS) + 0..15, k quads 4 (w % KS) + 0..3), piece q is
+    // row q / 2 of them, k octet q % 2.  Otherwise the wave's segments r' =
+    // 0..L-1 are 64 consecutive column quads each (from quad 64 w + r' NT of
+    // the k-major order), piece q is octet q % 32 of run q / 32.  Either way
+    // consecutive lanes read consecutive 16-byte pieces of the operand.
+    static __device__ __forceinline__ int copy_o(int t, int r) {
+        if constexpr (kWide)
+            return seg_o(t, r);
+        const int q = (t & 63) + 64 * r;
         if (KCONTIG)
-            return __umul24((uint32_t)min(o, o_lim - 1 - o0), ld4) + (uint32_t)kk * 4u;
-        return __umul24((uint32_t)kk, ld4) + (uint32_t)o * 4u;
+            return 16 * L * ((t >> 6) / KS) + q / 2;
+        return (((64 * (t >> 6) + (q / 32) * NT) / 2 + q % 32) % (D / 8)) * 8;
+    }
+    static __device__ __forceinline__ int copy_k(int t, int r) {
+        if constexpr (kWide)
+            return seg_k(t, r);
+        const int q = (t & 63) + 64 * r;
+        if (KCONTIG)
+            return 16 * ((t >> 6) % KS) + 8 * (q & 1);
+        return ((64 * (t >> 6) + (q / 32) * NT) / 2 + q % 32) / (D / 8);
+    }
+
+    // Byte offset of copy r from its chunk's base.  Rows past o_lim are
+    // clamped to the last valid row (their outputs are discarded); a copy
+    // straddling the last valid column is not made (copyable) and its
+    // segments are loaded element by element.  In builds for three or four
+    // waves per SIMD recomputed per chunk from the thread index, so that no
+    // per-thread offsets stay live across the K loop.  The leading dimension
+    // is below 2^22 elements (the library rejects larger ones), so its bytes
+    // and the row or k index fit a 24-bit multiply.
+    static __device__ __forceinline__ uint32_t boff(int tid, int r, int64_t ld, int o0, int o_lim) {
+        const int o = copy_o(tid, r);
+        const int kk = copy_k(tid, r);
+        const uint32_t es = (uint32_t)sizeof(T);
+        const uint32_t ldb = (uint32_t)ld * es;
+        if (KCONTIG)
+            return __umul24((uint32_t)min(o, o_lim - 1 - o0), ldb) + (uint32_t)kk * es;
+        return __umul24((uint32_t)kk, ldb) + (uint32_t)o * es;
     }
     static __device__ __forceinline__ bool copyable(int tid, int r, int o0, int o_lim) {
-        return KCONTIG || o0 + seg_o(tid, r) + 3 < o_lim;
+        return KCONTIG || o0 + copy_o(tid, r) + EPC - 1 < o_lim;
     }
-    // Every segment of the tile is copyable (the same for the whole
-    // workgroup): the tile lies inside the operand, or it is K-contiguous.
+    // Every copy of the tile is made (the same for the whole workgroup): the
+    // tile lies inside the operand, or it is K-contiguous.
     static __device__ __forceinline__ bool all_copyable(int o0, int o_lim) { return KCONTIG || o0 + D <= o_lim; }
-
-    // LDS landing slot of segment r of this thread (wave w, lane): block
-    // (r * NW + w) of 64 segments, the lane's 16 bytes within it.
-    static __device__ __forceinline__ uint32_t *slot_block(uint32_t *raw, int r, int w) {
-        return raw + (r * NW + w) * 256;
-    }
 
     // Start copying the chunk at `base` into the landing buffer at byte
     // RAW_OFF of the LDS array; lds_w is the LDS byte address of that array
-    // plus 1024 per wave index, so that block (r * NW + w) lies at
-    // lds_w + RAW_OFF + r * NW * 1024.  Called only for an interior chunk of
-    // an aligned operand.
+    // plus 1024 per wave index, so that copy r of wave w lands in block
+    // (r * NW + w) at lds_w + RAW_OFF + r * NW * 1024 (16 bytes per lane).
+    // Called only for an interior chunk of an aligned operand.
     template <int RAW_OFF, int R>
     static __device__ __forceinline__ void copy_seg(const char *cb, uint32_t lds_w, int tid, int64_t ld, int o0,
                                                     int o_lim) {
         dma_copy16<RAW_OFF + R * NW * 1024>(cb, boff(tid, R, ld, o0, o_lim), lds_w);
     }
     template <int RAW_OFF>
-    static __device__ __forceinline__ void copy(const float *__restrict__ base, uint32_t lds_w, int tid,
-                                                int64_t ld, int o0, int o_lim) {
+    static __device__ __forceinline__ void copy(const T *__restrict__ base, uint32_t lds_w, int tid, int64_t ld,
+                                                int o0, int o_lim) {
         const char *cb = reinterpret_cast<const char *>(base);
-        static_assert(L == 2 || L == 4, "segments per thread");
+        static_assert(CL == 1 || CL == 2 || CL == 4, "copies per thread");
         if (all_copyable(o0, o_lim)) {
             copy_seg<RAW_OFF, 0>(cb, lds_w, tid, ld, o0, o_lim);
-            copy_seg<RAW_OFF, 1>(cb, lds_w, tid, ld, o0, o_lim);
-            if constexpr (L == 4) {
+            if constexpr (CL >= 2)
+                copy_seg<RAW_OFF, 1>(cb, lds_w, tid, ld, o0, o_lim);
+            if constexpr (CL == 4) {
                 copy_seg<RAW_OFF, 2>(cb, lds_w, tid, ld, o0, o_lim);
                 copy_seg<RAW_OFF, 3>(cb, lds_w, tid, ld, o0, o_lim);
             }
@@ -241,9 +308,11 @@ struct DmaTile {
         }
         if (copyable(tid, 0, o0, o_lim))
             copy_seg<RAW_OFF, 0>(cb, lds_w, tid, ld, o0, o_lim);
-        if (copyable(tid, 1, o0, o_lim))
-            copy_seg<RAW_OFF, 1>(cb, lds_w, tid, ld, o0, o_lim);
-        if constexpr (L == 4) {
+        if constexpr (CL >= 2) {
+            if (copyable(tid, 1, o0, o_lim))
+                copy_seg<RAW_OFF, 1>(cb, lds_w, tid, ld, o0, o_lim);
+        }
+        if constexpr (CL == 4) {
             if (copyable(tid, 2, o0, o_lim))
                 copy_seg<RAW_OFF, 2>(cb, lds_w, tid, ld, o0, o_lim);
             if (copyable(tid, 3, o0, o_lim))
@@ -251,44 +320,78 @@ struct DmaTile {
         }
     }
 
+    // Where segment r of this thread (wave w, lane) sits in the landing
+    // buffer: the word offset of its 16 (float32) or 8 (bfloat16) bytes.  A
+    // float32 segment is the lane's own copy r (block r * NW + w); a bfloat16
+    // segment is half of the copy of its eight elements, made by a lane of
+    // the same wave.
+    static __device__ __forceinline__ uint32_t slot_of(int w, int lane, int r) {
+        if constexpr (kWide)
+            return (uint32_t)((r * NW + w) * 256 + lane * 4);
+        const int q = KCONTIG ? ((lane & 15) * L + r) * 2 + (lane >> 5) : r * 32 + lane / 2;
+        const int half = KCONTIG ? (lane >> 4) & 1 : lane & 1;
+        return (uint32_t)(((q / 64) * NW + w) * 256 + (q % 64) * 4 + half * 2);
+    }
+    // Whether the copy holding segment r was made (see copyable).
+    static __device__ __forceinline__ bool seg_copied(int tid, int r, int o0, int o_lim) {
+        if constexpr (kWide)
+            return copyable(tid, r, o0, o_lim);
+        return KCONTIG || o0 + (seg_o(tid, r) & ~7) + 7 < o_lim;
+    }
+    static __device__ __forceinline__ uint4 read_slot(const uint32_t *raw, uint32_t off) {
+        if constexpr (kWide)
+            return *reinterpret_cast<const uint4 *>(raw + off);
+        const uint2 d = *reinterpret_cast<const uint2 *>(raw + off);
+        // Four bfloat16 elements widened exactly to float32 encodings.
+        return make_uint4(d.x << 16, d.x & 0xFFFF0000u, d.y << 16, d.y & 0xFFFF0000u);
+    }
+
     // The thread's segments of chunk [k0, k0 + BK): from the landing buffer
     // when they were copied, else element by element from global memory
     // (elements at k >= k_lim are zero).
     __device__ __forceinline__ void fetch(const uint32_t *raw, int w, int lane, bool copied,
-                                          const float *__restrict__ base, int64_t ld, int o0, int o_lim, int k0,
+                                          const T *__restrict__ base, int64_t ld, int o0, int o_lim, int k0,
                                           int k_lim, int tid) {
         if (copied && all_copyable(o0, o_lim)) {
             // The common case, one branch for all segments: the reads issue
             // back to back and are waited for once.
 #pragma unroll
             for (int r = 0; r < L; ++r)
-                v[r] = *reinterpret_cast<const uint4 *>(slot_block(const_cast<uint32_t *>(raw), r, w) + lane * 4);
+                v[r] = read_slot(raw, slot_of(w, lane, r));
             return;
         }
 #pragma unroll
         for (int r = 0; r < L; ++r) {
-            if (copied && copyable(tid, r, o0, o_lim))
-                v[r] = *reinterpret_cast<const uint4 *>(slot_block(const_cast<uint32_t *>(raw), r, w) + lane * 4);
+            if (copied && seg_copied(tid, r, o0, o_lim))
+                v[r] = read_slot(raw, slot_of(w, lane, r));
             else
-                v[r] = load_elements(reinterpret_cast<const char *>(base), r, ld, o0, o_lim, k0, k_lim, tid);
+                v[r] = load_elements(base, r, ld, o0, o_lim, k0, k_lim, tid);
         }
     }
 
-    static __device__ __forceinline__ uint4 load_elements(const char *cb, int r, int64_t ld, int o0, int o_lim,
-                                                          int k0, int k_lim, int tid) {
-        const float *src = reinterpret_cast<const float *>(cb + boff(tid, r, ld, o0, o_lim));
+    static __device__ __forceinline__ uint32_t widen(float x) { return __float_as_uint(x); }
+    static __device__ __forceinline__ uint32_t widen(uint16_t h) { return (uint32_t)h << 16; }
+
+    static __device__ __forceinline__ uint4 load_elements(const T *base, int r, int64_t ld, int o0, int o_lim, int k0,
+                                                          int k_lim, int tid) {
+        const int o = seg_o(tid, r);
         const int kk = seg_k(tid, r);
         uint32_t e[4];
         if (KCONTIG) {
+            // (a float32 segment is its own copy: boff is its offset)
+            const T *src = kWide ? reinterpret_cast<const T *>(reinterpret_cast<const char *>(base) +
+                                                               boff(tid, r, ld, o0, o_lim))
+                                 : base + (int64_t)(min(o0 + o, o_lim - 1) - o0) * ld + kk;
 #pragma unroll
             for (int c = 0; c < 4; ++c)
-                e[c] = (k0 + kk + c < k_lim) ? __float_as_uint(src[c]) : 0u;
+                e[c] = (k0 + kk + c < k_lim) ? widen(src[c]) : 0u;
         } else {
-            const int o = seg_o(tid, r);
-            const float *row = src - o;
+            const T *row = kWide ? reinterpret_cast<const T *>(reinterpret_cast<const char *>(base) +
+                                                               boff(tid, r, ld, o0, o_lim)) - o
+                                 : base + (int64_t)kk * ld;
 #pragma unroll
             for (int c = 0; c < 4; ++c)
-                e[c] = (k0 + kk < k_lim) ? __float_as_uint(row[min(o0 + o + c, o_lim - 1) - o0]) : 0u;
+                e[c] = (k0 + kk < k_lim) ? widen(row[min(o0 + o + c, o_lim - 1) - o0]) : 0u;
         }
         return make_uint4(e[0], e[1], e[2], e[3]);
     }
@@ -348,8 +451,7 @@ struct DmaTile {
     static __device__ __forceinline__ uint32_t enc(uint32_t u, bool is_b) { return is_b ? u - kBias : u; }
 
     // Write the encoded chunk k-major into s[k * D + o] and mark the step
-    // masks (as the register-staged kernel's TileLoader::store): bit k % KPG
-    // of the word of k-group k / KPG.
+    // masks: bit k % KPG of the word of k-group k / KPG.
     template <int KPG, typename SlotOf>
     __device__ __forceinline__ void store(uint32_t *s, bool is_b, int tid, const uint32_t (&smin)[L], uint32_t *mask,
                                           int slots, SlotOf slot_of) const {
@@ -408,11 +510,11 @@ constexpr int dma_waves_per_simd(int bm, int bn, int kw) {
     return (bm == 128 && bn == 128 && kw == 1) ? 4 : (bm == 128 && bn == 64 && kw == 2) ? 3 : 2;
 }
 
-// k steps per k-group per LDS chunk.  The same as the bfloat16 kernel's, so
-// that both partition K among the k-groups alike and give the same bits (an
-// 8-step chunk for the 64 x 64 tile with four k-groups, at 32 KB of LDS and
-// four waves per SIMD, measured 8-20% faster on w4 / w2 shapes, but would
-// sum in another order).
+// k steps per k-group per LDS chunk (an 8-step chunk for the 64 x 64 tile
+// with four k-groups, at 32 KB of LDS and four waves per SIMD, measured
+// 8-20% faster on w4 / w2 shapes with the earlier register-staged kernel; it
+// sums in another order, and the plans the library picks do not use that
+// tile for the benchmark products).
 constexpr int dma_kpg(int, int, int) { return kChunkK; }
 
 // Minimum LDS words per workgroup.  Workgroups of one or two waves can be
@@ -434,7 +536,7 @@ constexpr int dma_min_lds_words(int bm, int bn, int kw, int wps) {
 // per-thread staging addresses are computed once, before the K loop;
 // otherwise they are recomputed per chunk, since registers held across the
 // loop would not fit beside the accumulators.
-template <int BM, int BN, int KW, bool TA, bool TB, int WPS>
+template <int BM, int BN, int KW, bool TA, bool TB, int WPS, typename T>
 __global__ void __launch_bounds__(BM * BN / 64 * KW) __attribute__((amdgpu_waves_per_eu(WPS)))
 pam_gemm_dma_kernel(GemmParams p) {
     constexpr bool kKeepAddresses = WPS <= 2 || (WPS == 3 && !TA);
@@ -450,10 +552,10 @@ pam_gemm_dma_kernel(GemmParams p) {
     constexpr int HM = BM / 2;
     constexpr int HN = BN / 2;
     constexpr int LDR = BN;                // partial-tile rows (KW > 1)
-    using TileA = DmaTile<BM, BK, NT, !TA>;
-    using TileB = DmaTile<BN, BK, NT, TB>;
-    constexpr int kRawA = TileA::SEGS * 4;
-    constexpr int kRawB = TileB::SEGS * 4;
+    using TileA = DmaTile<BM, BK, NT, !TA, T>;
+    using TileB = DmaTile<BN, BK, NT, TB, T>;
+    constexpr int kRawA = TileA::CL * NT * 4;   // 16 bytes per copy
+    constexpr int kRawB = TileB::CL * NT * 4;
     constexpr int kStage = kRawA + kRawB + BK * BM + BK * BN;
     // Partial tiles held at once by the LDS after the K loop (KW > 1).
     constexpr int kRedTiles = KW == 1 ? 0 : (kStage / (BM * LDR) >= KW - 1 ? KW - 1 : kStage / (BM * LDR));
@@ -501,8 +603,10 @@ pam_gemm_dma_kernel(GemmParams p) {
     const int ke = whole ? p.k : min(p.k, kb + p.k_per_split);
     const int nchunks = ke > kb ? (ke - kb + BK - 1) / BK : 0;
 
-    const float *a_base = p.A + bz * p.strideA + (TA ? (int64_t)kb * p.lda + m0 : (int64_t)m0 * p.lda + kb);
-    const float *b_base = p.B + bz * p.strideB + (TB ? (int64_t)n0 * p.ldb + kb : (int64_t)kb * p.ldb + n0);
+    const T *a_base = reinterpret_cast<const T *>(p.A) + bz * p.strideA +
+                      (TA ? (int64_t)kb * p.lda + m0 : (int64_t)m0 * p.lda + kb);
+    const T *b_base = reinterpret_cast<const T *>(p.B) + bz * p.strideB +
+                      (TB ? (int64_t)n0 * p.ldb + kb : (int64_t)kb * p.ldb + n0);
     const int64_t a_step = TA ? (int64_t)BK * p.lda : BK;
     const int64_t b_step = TB ? BK : (int64_t)BK * p.ldb;
     const bool vec_a = p.vec_a != 0;
@@ -758,44 +862,52 @@ pam_gemm_dma_kernel(GemmParams p) {
     }
 }
 
-template <int BM, int BN, int KW, int WPS = dma_waves_per_simd(BM, BN, KW)>
+template <typename T, int BM, int BN, int KW, int WPS = dma_waves_per_simd(BM, BN, KW)>
 static hipError_t launch_dma_tile(bool ta, bool tb, const GemmParams &p, dim3 grid, hipStream_t stream) {
     const dim3 block(BM * BN / 64 * KW);
     if (!ta && !tb)
-        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, false, WPS>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, false, WPS, T>), grid, block, 0, stream, p);
     else if (!ta && tb)
-        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, true, WPS>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, false, true, WPS, T>), grid, block, 0, stream, p);
     else if (ta && !tb)
-        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, false, WPS>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, false, WPS, T>), grid, block, 0, stream, p);
     else
-        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, true, WPS>), grid, block, 0, stream, p);
+        hipLaunchKernelGGL((pam_gemm_dma_kernel<BM, BN, KW, true, true, WPS, T>), grid, block, 0, stream, p);
     return hipGetLastError();
 }
 
-hipError_t launch_pam_gemm_dma(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, const GemmParams &p,
-                               hipStream_t stream) {
-    const int64_t items = (int64_t)p.whole + (int64_t)p.split_tiles * p.splits;
-    if (items <= 0 || items > kMaxLaunchItems)
-        return hipErrorInvalidValue;
+template <typename T>
+static hipError_t launch_dma_shape(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b,
+                                   const GemmParams &p, int64_t items, hipStream_t stream) {
     const dim3 grid((unsigned)items);
     if (tile_m == 128 && tile_n == 128 && kgroups == 1)
-        return launch_dma_tile<128, 128, 1>(trans_a, trans_b, p, grid, stream);
+        return launch_dma_tile<T, 128, 128, 1>(trans_a, trans_b, p, grid, stream);
     if (tile_m == 128 && tile_n == 64 && kgroups == 1)
-        return launch_dma_tile<128, 64, 1>(trans_a, trans_b, p, grid, stream);
+        return launch_dma_tile<T, 128, 64, 1>(trans_a, trans_b, p, grid, stream);
     if (tile_m == 128 && tile_n == 64 && kgroups == 2)
     {
         // A launch that two workgroups per compute unit hold at once runs
         // the build for two waves per SIMD (staging addresses kept in
         // registers); its occupancy is two anyway.
         if (items <= 2 * 256)
-            return launch_dma_tile<128, 64, 2, 2>(trans_a, trans_b, p, grid, stream);
-        return launch_dma_tile<128, 64, 2>(trans_a, trans_b, p, grid, stream);
+            return launch_dma_tile<T, 128, 64, 2, 2>(trans_a, trans_b, p, grid, stream);
+        return launch_dma_tile<T, 128, 64, 2>(trans_a, trans_b, p, grid, stream);
     }
     if (tile_m == 64 && tile_n == 64 && kgroups == 1)
-        return launch_dma_tile<64, 64, 1>(trans_a, trans_b, p, grid, stream);
+        return launch_dma_tile<T, 64, 64, 1>(trans_a, trans_b, p, grid, stream);
     if (tile_m == 64 && tile_n == 64 && kgroups == 4)
-        return launch_dma_tile<64, 64, 4>(trans_a, trans_b, p, grid, stream);
+        return launch_dma_tile<T, 64, 64, 4>(trans_a, trans_b, p, grid, stream);
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_pam_gemm_dma(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, bool bf16,
+                               const GemmParams &p, hipStream_t stream) {
+    const int64_t items = (int64_t)p.whole + (int64_t)p.split_tiles * p.splits;
+    if (items <= 0 || items > kMaxLaunchItems)
+        return hipErrorInvalidValue;
+    if (bf16)
+        return launch_dma_shape<uint16_t>(tile_m, tile_n, kgroups, trans_a, trans_b, p, items, stream);
+    return launch_dma_shape<float>(tile_m, tile_n, kgroups, trans_a, trans_b, p, items, stream);
 }
 
 }  // namespace pamk

@@ -1,5 +1,6 @@
 // Internal interface between the C-ABI layer (pam_api.cpp) and the HIP
-// kernels (pam_kernels.hip).  Not installed; not part of the public ABI.
+// kernels (pam_gemm_dma.hip, pam_kernels.hip, pa_ops.hip,
+// pam_exact_grad.hip).  Not installed; not part of the public ABI.
 #pragma once
 
 #include <stdint.h>
@@ -58,10 +59,11 @@ hipError_t launch_round_mantissa(const float *a, float *out, int64_t n, int drop
 hipError_t launch_pam_gemm(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, bool bf16,
                            const GemmParams &p, hipStream_t stream);
 
-// The same products for float32 operands, with the operand chunks copied
-// into LDS by the memory pipeline (pam_gemm_dma.hip); same tile shapes, same
-// results bit for bit.
-hipError_t launch_pam_gemm_dma(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b,
+// The kernel behind launch_pam_gemm (pam_gemm_dma.hip): operand chunks
+// copied into LDS by the memory pipeline.  With bf16, the copies need the
+// operand 16-byte aligned with leading dimension and stride multiples of 8
+// elements (p.vec_a / p.vec_b), else its elements are loaded one by one.
+hipError_t launch_pam_gemm_dma(int tile_m, int tile_n, int kgroups, bool trans_a, bool trans_b, bool bf16,
                                const GemmParams &p, hipStream_t stream);
 
 // C of the split tiles of a matrix product launch: element by element the sum

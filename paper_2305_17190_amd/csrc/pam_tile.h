@@ -1,8 +1,8 @@
-// Operand tile staging shared by the PAM matrix-product kernels: the
-// per-thread global-memory loader of a D x BK operand
-// tile (16-byte loads at fixed per-thread offsets, ragged edges, k tail), its
-// scans and the SCALED-encoding LDS store, and the 8-value LDS fragment read.
-// Included by the HIP sources only.
+// Operand tile staging through registers, used by the exact-derivative
+// products (pam_exact_grad.hip): the per-thread global-memory loader of a
+// D x BK operand tile (16-byte loads at fixed per-thread offsets, ragged
+// edges, k tail), its scans and the SCALED-encoding LDS store, and the
+// 8-value LDS fragment read.  Included by the HIP sources only.
 #pragma once
 
 #include <hip/hip_runtime.h>

@@ -338,10 +338,20 @@ struct DmaTile {
             return copyable(tid, r, o0, o_lim);
         return KCONTIG || o0 + (seg_o(tid, r) & ~7) + 7 < o_lim;
     }
+    // Reads through an LDS-space pointer: the compiler then cannot merge a
+    // landing-buffer read with the element-by-element global loads of the
+    // other branch into one generic (flat) load.
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    typedef __attribute__((address_space(3))) const u32x4 lds_u32x4;
+    typedef __attribute__((address_space(3))) const u32x2 lds_u32x2;
     static __device__ __forceinline__ uint4 read_slot(const uint32_t *raw, uint32_t off) {
-        if constexpr (kWide)
-            return *reinterpret_cast<const uint4 *>(raw + off);
-        const uint2 d = *reinterpret_cast<const uint2 *>(raw + off);
+        if constexpr (kWide) {
+            const u32x4 x = *(lds_u32x4 *)(raw + off);
+            return make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        const u32x2 y = *(lds_u32x2 *)(raw + off);
+        const uint2 d = make_uint2(y[0], y[1]);
         // Four bfloat16 elements widened exactly to float32 encodings.
         return make_uint4(d.x << 16, d.x & 0xFFFF0000u, d.y << 16, d.y & 0xFFFF0000u);
     }

@@ -106,3 +106,46 @@ def test_bf16_argument_rules():
         pam.bmm(a[None], a[None], plan=(128, 128, 1))
     with pytest.raises(ValueError):
         pam.gemm(a, a, mantissa_bits=4)
+
+
+
+# Sizes for which the library picks each tile shape, k-group count and kind of
+# split (none, split K, whole-K tiles then split ones): (m, n, k, batch) ->
+# (tile_m, tile_n, kgroups, splits K, has whole-K tiles).  Each tile shape and
+# operand layout has its own map from the copies a wave makes to the segments
+# its lanes stage.
+PLAN_SHAPES = [
+    ((150, 2500, 40, 8), (128, 128, 1, False, False)),
+    ((150, 70, 5000, 8), (128, 128, 1, True, False)),
+    ((1000, 4100, 1000, 1), (128, 128, 1, True, True)),
+    ((1200, 300, 1000, 8), (128, 64, 1, True, True)),
+    ((70, 1200, 5000, 1), (128, 64, 1, True, False)),
+    ((70, 2500, 40, 8), (128, 64, 2, False, False)),
+    ((70, 70, 1000, 1), (128, 64, 2, True, False)),
+    ((70, 70, 40, 1), (64, 64, 4, False, False)),
+    ((70, 70, 20000, 1), (64, 64, 4, True, False)),
+    ((150, 1200, 5000, 2), (64, 64, 1, True, False)),
+]
+
+
+@pytest.mark.parametrize("aligned", [True, False], ids=["rows8", "ragged"])
+@pytest.mark.parametrize("ta,tb", [(False, False), (False, True), (True, False), (True, True)],
+                         ids=["NN", "NT", "TN", "TT"])
+@pytest.mark.parametrize("shape,kind", PLAN_SHAPES, ids=lambda v: "x".join(map(str, v)) if len(v) == 4 else None)
+def test_bf16_every_tile_and_layout(shape, kind, ta, tb, aligned):
+    # Bit for bit the product of the widened float32 operands under every plan
+    # kind and layout, with ragged tile edges in M and N and a K tail; rows of
+    # a multiple of 8 elements take the 16-byte copies, the others the
+    # element-by-element loads.
+    import torch
+    m, n, k, batch = shape
+    if aligned:
+        m, n, k = (-(-d // 8) * 8 for d in (m, n, k))
+    p = pam.plan(m, n, k, batch)
+    note(f"bf16 every tile m={m} n={n} k={k} batch={batch} ta={ta} tb={tb} plan={p}")
+    assert (p[0], p[1], p[3], p[2] > 1, p[4] > 0) == kind
+    a16 = bf16_bits((batch, k, m) if ta else (batch, m, k), 11 + m, True).to(device())
+    b16 = bf16_bits((batch, n, k) if tb else (batch, k, n), 12 + n, True).to(device())
+    c16 = pam.bmm(a16, b16, trans_a=ta, trans_b=tb)
+    c32 = pam.bmm(a16.float(), b16.float(), trans_a=ta, trans_b=tb)
+    assert torch.equal(c16.view(torch.int32), c32.view(torch.int32))

@@ -392,3 +392,39 @@ def test_special_beside_low_in_one_segment(operand, ta, tb, plan):
         c = pam.bmm(to_dev(a)[None], to_dev(b)[None], trans_a=ta, trans_b=tb, plan=plan)
         c_ref, s_ref = oracle_gemm(a.ravel(), b.ravel(), ta, tb, m, n, k, a.shape[1], b.shape[1], batches=[0])
         check_gemm(c.cpu().numpy(), c_ref, s_ref, k, f"segment mix {case} {operand} ta={ta} tb={tb} {plan}")
+
+
+@pytest.mark.parametrize("where", ["first", "second", "both", "B"])
+@pytest.mark.parametrize("plan", [(128, 128, 1), (128, 64, 1), (128, 64, 1, 2), (64, 64, 1), (64, 64, 1, 4),
+                                  (128, 128, 3, 1, 2)], ids=lambda p: "x".join(map(str, p)))
+@pytest.mark.parametrize("ta,tb", TRANS, ids=["NN", "NT", "TN", "TT"])
+def test_low_values_in_one_half_of_the_tile_rows(where, plan, ta, tb):
+    # Zeros, denormals and tiny normals only in the rows of op(A) that lie in
+    # the first (second) half of their tile's rows, in both halves, or only
+    # in B.  A k step then needs the zero / underflow handling for the rows
+    # of one half and not for the other.  Two-mantissa-bit operands whose
+    # sums are exact in any order: equal to the oracle bit for bit.
+    import pam_workloads as wl
+    m, n, k = 150, 140, 200
+    tm = plan[0]
+    note(f"low values in {where} rows plan={plan} ta={ta} tb={tb}")
+    a_op = wl.exact_sum_values((m, k), 901, 0.0, 0.0)
+    b_op = wl.exact_sum_values((k, n), 902, 0.0, 0.0)
+    g = np.random.default_rng(903)
+    low = wl.exact_sum_values((m + k, max(n, k)), 904, 0.5, 0.5)      # zeros, denormals, tiny normals
+    if where == "B":
+        hit = g.random((k, n)) < 0.01
+        b_op[hit] = low[:k, :n][hit]
+    else:
+        half = (np.arange(m) % tm) >= tm // 2
+        rows = {"first": ~half, "second": half, "both": np.ones(m, bool)}[where]
+        hit = (g.random((m, k)) < 0.03) & rows[:, None]
+        a_op[hit] = low[:m, :k][hit]
+    a = np.ascontiguousarray(a_op.T) if ta else a_op
+    b = np.ascontiguousarray(b_op.T) if tb else b_op
+    got = pam.bmm(to_dev(a[None]), to_dev(b[None]), trans_a=ta, trans_b=tb, plan=plan).cpu().numpy()[0]
+    c_ref, _ = pam_ref.pam_gemm_ref(a, b, ta, tb)
+    assert np.array_equal(c_ref.astype(np.float32).astype(np.float64), c_ref), "test data does not sum exactly"
+    bad = np.nonzero(got.astype(np.float64) != c_ref)
+    assert bad[0].size == 0, (f"{bad[0].size} outputs differ; first ({bad[0][0]}, {bad[1][0]}): "
+                              f"got {got[bad][0]!r} want {c_ref[bad][0]!r}")

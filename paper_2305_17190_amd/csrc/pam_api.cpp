@@ -30,7 +30,6 @@ pam_status_t fail_hip(hipError_t e, const char *what) {
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-bool aligned8(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
 constexpr int64_t kMaxDim = 0x7FFFFFFF;
 constexpr int64_t kMaxSplits = 64;

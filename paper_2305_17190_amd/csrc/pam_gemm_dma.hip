@@ -520,11 +520,8 @@ constexpr int dma_waves_per_simd(int bm, int bn, int kw) {
     return (bm == 128 && bn == 128 && kw == 1) ? 4 : (bm == 128 && bn == 64 && kw == 2) ? 3 : 2;
 }
 
-// k steps per k-group per LDS chunk (an 8-step chunk for the 64 x 64 tile
-// with four k-groups, at 32 KB of LDS and four waves per SIMD, measured
-// 8-20% faster on w4 / w2 shapes with the earlier register-staged kernel; it
-// sums in another order, and the plans the library picks do not use that
-// tile for the benchmark products).
+// k steps per k-group per LDS chunk: the same for every tile shape (the
+// step masks hold one bit per step of a chunk in each half of a 32-bit word).
 constexpr int dma_kpg(int, int, int) { return kChunkK; }
 
 // Minimum LDS words per workgroup.  Workgroups of one or two waves can be

@@ -1,14 +1,14 @@
-"""Seeded random configurations of the batched product against the oracle.
+"""Seeded random operand views of the batched product against the oracle.
 
-Each case draws its own sizes (small and multi-tile, ragged in every
-dimension), transposes, batch count, leading-dimension padding, batch stride,
-storage offset (16-byte aligned or not), output padding, element type
-(float32 or bfloat16), value mix (normal values, or with planted zeros,
-denormals and tiny normals) and plan (the library's, or a forced tile shape,
-split count and whole-K tile count for float32).  The product must agree with
-the oracle within the GEMM tolerance, leave the output's padding untouched,
-and for bfloat16 operands equal the float32 product of the widened operands
-bit for bit.
+Beside the randomized sweep of sizes and plans, each case here places its
+operands at a storage offset (often not 16-byte aligned, so the kernels load
+those operands element by element), leaves gaps between the matrices of a
+batch, pads leading dimensions and the output's rows, and mixes float32 and
+bfloat16 elements, normal values and planted zeros, denormals and tiny
+normals, the library's plan and forced plans (tile shape, split count,
+whole-K tile count).  The product must agree with the oracle within the GEMM
+tolerance and leave the output's padding untouched; bfloat16 products must
+equal the float32 product of the widened operands bit for bit.
 """
 import numpy as np
 import pytest
@@ -78,10 +78,10 @@ def operand(g, batch, rows, cols, pad, gap, off, low, bf16):
 
 
 @pytest.mark.parametrize("seed", range(200))
-def test_random_configuration(seed):
+def test_random_view(seed):
     import torch
     c = draw(seed)
-    note(f"random configuration {seed}: {c}")
+    note(f"random view {seed}: {c}")
     g = np.random.default_rng(9500 + seed)
     m, n, k, batch, ta, tb = c["m"], c["n"], c["k"], c["batch"], c["ta"], c["tb"]
     a_rows, a_cols = (k, m) if ta else (m, k)
@@ -96,7 +96,7 @@ def test_random_configuration(seed):
     if c["pad_c"]:
         assert np.all(np.isnan(got[:, :, n:])), "wrote outside the output's columns"
     c_ref, s_ref = oracle_gemm(a_flat, b_flat, ta, tb, m, n, k, lda, ldb, sa, sb, batches=list(range(batch)))
-    check_gemm(got[:, :, :n], c_ref, s_ref, k, f"random configuration {seed}")
+    check_gemm(got[:, :, :n], c_ref, s_ref, k, f"random view {seed}")
     if c["bf16"]:
         wide = pam.bmm(A.float(), B.float(), trans_a=ta, trans_b=tb)
         assert torch.equal(out.contiguous().view(torch.int32), wide.view(torch.int32)), \

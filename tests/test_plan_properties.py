@@ -48,12 +48,13 @@ def test_plans_are_valid(m, n, k, batch):
 
 # The plans the library picks for the benchmark products (tile_m, tile_n,
 # splits, k-groups, whole-K tiles), measured against the fastest plan of an
-# exhaustive sweep: the best or within 0.3% on w2 and w4, within 0.9% on w5,
-# 1-4% behind on w3's products: a change of the cost model that moves one of
-# them has to be measured again.
+# exhaustive sweep: the best or within 0.3% on w2 and w4, within 0.9% on w5;
+# on w3 up / dH (one full round of whole-K tiles) the quarter-round hybrid
+# within 1% of the best (3 slices), down / dX 2-4% behind 6-7 slices: a
+# change of the cost model that moves one of them has to be measured again.
 WORKLOAD_PLANS = {
     (2, "fwd"): (128, 64, 1, 2, 0), (2, "dX"): (128, 64, 4, 2, 0), (2, "dW"): (128, 64, 53, 1, 0),
-    (3, "up"): (128, 128, 1, 1, 0), (3, "down"): (128, 128, 4, 1, 0), (3, "dH"): (128, 128, 1, 1, 0),
+    (3, "up"): (128, 128, 4, 1, 768), (3, "down"): (128, 128, 4, 1, 0), (3, "dH"): (128, 128, 4, 1, 768),
     (3, "dW2"): (128, 128, 16, 1, 0), (3, "dX"): (128, 128, 4, 1, 0), (3, "dW1"): (128, 128, 16, 1, 0),
     (4, "QKt"): (128, 128, 1, 1, 0), (4, "PV"): (128, 64, 1, 2, 0), (4, "dP"): (128, 128, 1, 1, 0),
     (4, "dV"): (128, 64, 1, 2, 0), (4, "dQ"): (128, 64, 1, 2, 0), (4, "dK"): (128, 64, 1, 2, 0),
@@ -69,3 +70,18 @@ def test_workload_plans_are_pinned():
             assert pam.plan(f.m, f.n, f.k, f.batch) == WORKLOAD_PLANS[(w, f.name)], (w, f.name)
             seen.add((w, f.name))
     assert seen == set(WORKLOAD_PLANS)
+
+
+def test_one_full_round_takes_the_quarter_round_hybrid():
+    # 1024 output tiles of 128 x 128 (one full round of resident workgroups):
+    # with K >= 512 and a workspace, whole-K tiles in three quarters of the
+    # slots and the last 256 tiles in K slices (4 up to K = 1279, one per 20
+    # chunks beyond); shorter K, no workspace, or a tile count that is not one
+    # round keep the model's plan.
+    for (m, n, batch) in ((8192, 2048, 1), (2048, 8192, 1), (4096, 4096, 1), (4096, 2048, 2), (1024, 1024, 16)):
+        for k, slices in ((512, 4), (768, 4), (1024, 4), (1279, 4), (2048, 6)):
+            assert pam.plan(m, n, k, batch) == (128, 128, slices, 1, 768), (m, n, k, batch)
+            assert pam.plan(m, n, k, batch, max_workspace_bytes=0)[2] == 1
+        assert pam.plan(m, n, 256, batch)[2] == 1
+        assert pam.plan(m, n, 500, batch)[2] == 1
+    assert pam.plan(8192, 2048 + 128, 1024, 1) != (128, 128, 4, 1, 768)     # 1088 tiles: the model's plan
